@@ -1,0 +1,170 @@
+"""Seeded synthetic q/k/v generator and the named workload shapes.
+
+Every tensor is drawn from ``numpy.random.default_rng`` keyed by a
+``SeedSequence`` built from (base seed, workload id, batch index, chunk index,
+denoising step, layer, tensor id), so any single chunk of any stream can be
+regenerated on its own. Values are N(0, 1) in fp32; queries and keys are then
+divided by their root-mean-square over the head dimension (one row per token
+and head, no gain, no epsilon); for bfloat16 workloads every value is rounded
+to nearest-even bfloat16 and handed out both as raw 16-bit patterns (for upload
+to the device) and as the exactly equal fp32 values (for the CPU side).
+
+Layout of every tensor: ``[n_tokens, heads, head_dim]`` for one batch element;
+callers stack batch elements in front to get ``[B, L, H, D]``.
+
+The latent shapes follow the WAN2.1-14B image-to-video backbone the paper
+builds on (Sec. 4.1): 40 heads of width 128, a 16x spatial patch grid per
+latent frame (480x832 -> 30x52 = 1560 tokens, 720x1280 -> 45x80 = 3600), and
+the paper's chunking of the 21-latent-frame clip into chunks of 3 latent
+frames (Sec. 4.2, chunked processing).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+TENSOR_Q, TENSOR_K, TENSOR_V = 0, 1, 2
+FULL_SEQUENCE_CHUNK = 1000  # seed slot used when a whole sequence is drawn at once
+
+
+@dataclass(frozen=True)
+class Workload:
+    """Shape of one synthetic workload.
+
+    tokens_per_frame (T), chunk_frames (C), ref_frames (R) and window (W)
+    describe the chunk geometry; ``n_frames`` is the sequence length in latent
+    frames for the full-sequence form; ``n_chunks`` the number of streamed
+    chunks for the streaming form.
+    """
+
+    wid: int
+    name: str
+    dtype: str  # "f32" or "bf16"
+    batch: int
+    heads: int
+    head_dim: int
+    tokens_per_frame: int
+    chunk_frames: int
+    ref_frames: int
+    window: int
+    n_frames: int = 0
+    n_chunks: int = 0
+    steps: int = 1
+    layers: int = 1
+    notes: str = field(default="", compare=False)
+
+    @property
+    def chunk_tokens(self) -> int:
+        return self.chunk_frames * self.tokens_per_frame
+
+    @property
+    def ref_tokens(self) -> int:
+        return self.ref_frames * self.tokens_per_frame
+
+
+WORKLOADS: dict[str, Workload] = {
+    w.name: w
+    for w in [
+        Workload(1, "tiny_f32", "f32", 1, 2, 64, 64, 2, 1, 1, n_frames=9, n_chunks=4,
+                 notes="64 tokens/frame, chunk of 2 frames, 4 streamed chunks"),
+        Workload(2, "wan14b_480p_chunk", "bf16", 1, 40, 128, 1560, 3, 1, 1, n_chunks=2,
+                 notes="one 4680-query chunk over 1560 ref + 4680 previous + 4680 current keys"),
+        Workload(3, "wan14b_480p_full_sequence", "bf16", 1, 40, 128, 1560, 3, 1, 1, n_frames=21,
+                 notes="21 latent frames: reference frame + six 3-frame chunks + one 2-frame chunk"),
+        Workload(4, "wan14b_480p_stream", "bf16", 1, 40, 128, 1560, 3, 1, 1, n_chunks=10,
+                 steps=2, layers=40,
+                 notes="10 chunks x 2 denoising steps x 40 layers of append + attention"),
+        Workload(5, "wan14b_720p_chunk_b2", "bf16", 2, 40, 128, 3600, 3, 1, 1, n_chunks=2,
+                 notes="two independent streams, one 10800-query chunk over 25200 keys each"),
+    ]
+}
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 to bfloat16, nearest-even, returning the 16-bit patterns.
+
+    Finite inputs only (the generator never produces inf/NaN).
+    """
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    rounded = u + np.uint32(0x7FFF) + lsb
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns to fp32."""
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _rng(wid: int, b: int, chunk: int, step: int, layer: int, tensor_id: int,
+         base_seed: int = 0) -> np.random.Generator:
+    return np.random.default_rng(
+        np.random.SeedSequence([base_seed, wid, b, chunk, step, layer, tensor_id]))
+
+
+def draw_tensor(shape, *, wid: int, b: int, chunk: int, step: int, layer: int,
+                tensor_id: int, rms_normalise: bool, dtype: str, base_seed: int = 0):
+    """Draw one seeded tensor of ``shape`` (last axis = head_dim).
+
+    Returns ``(f32_values, bf16_bits_or_None)``. For ``dtype == "bf16"`` the
+    fp32 array holds exactly the bfloat16 values whose bit patterns are
+    returned alongside.
+    """
+    x = _rng(wid, b, chunk, step, layer, tensor_id, base_seed).standard_normal(
+        size=shape, dtype=np.float32)
+    if rms_normalise:
+        x /= np.sqrt(np.mean(x * x, axis=-1, keepdims=True, dtype=np.float32))
+    if dtype == "f32":
+        return x, None
+    if dtype != "bf16":
+        raise ValueError(f"unknown dtype {dtype!r}")
+    bits = f32_to_bf16_bits(x)
+    return bf16_bits_to_f32(bits), bits
+
+
+def _draw_qkv(n_tok: int, w: Workload, b: int, chunk: int, step: int, layer: int,
+              base_seed: int):
+    shape = (n_tok, w.heads, w.head_dim)
+    out = []
+    for tid in (TENSOR_Q, TENSOR_K, TENSOR_V):
+        out.append(draw_tensor(shape, wid=w.wid, b=b, chunk=chunk, step=step, layer=layer,
+                               tensor_id=tid, rms_normalise=tid != TENSOR_V, dtype=w.dtype,
+                               base_seed=base_seed))
+    return out
+
+
+def draw_chunk(w: Workload, chunk: int, n_tok: int | None = None, *, step: int = 0,
+               layer: int = 0, base_seed: int = 0):
+    """q, k, v for one chunk of every batch element, shaped ``[B, n_tok, H, D]``.
+
+    ``chunk == 0`` is the reference chunk (``R*T`` tokens by default), later
+    chunks hold ``C*T`` tokens unless ``n_tok`` says otherwise.
+    Returns a dict with fp32 arrays ``q, k, v`` and, for bf16 workloads, the
+    bit patterns ``q_bits, k_bits, v_bits`` (uint16).
+    """
+    if n_tok is None:
+        n_tok = w.ref_tokens if chunk == 0 else w.chunk_tokens
+    per_b = [_draw_qkv(n_tok, w, b, chunk, step, layer, base_seed) for b in range(w.batch)]
+    res = {}
+    for i, name in enumerate("qkv"):
+        res[name] = np.stack([pb[i][0] for pb in per_b])
+        if w.dtype == "bf16":
+            res[name + "_bits"] = np.stack([pb[i][1] for pb in per_b])
+    return res
+
+
+def draw_qkv_sequence(w: Workload, n_frames: int | None = None, *, step: int = 0,
+                      layer: int = 0, base_seed: int = 0):
+    """q, k, v for a whole ``n_frames``-frame sequence, shaped ``[B, L, H, D]``."""
+    if n_frames is None:
+        n_frames = w.n_frames
+    n_tok = n_frames * w.tokens_per_frame
+    per_b = [_draw_qkv(n_tok, w, b, FULL_SEQUENCE_CHUNK, step, layer, base_seed)
+             for b in range(w.batch)]
+    res = {}
+    for i, name in enumerate("qkv"):
+        res[name] = np.stack([pb[i][0] for pb in per_b])
+        if w.dtype == "bf16":
+            res[name + "_bits"] = np.stack([pb[i][1] for pb in per_b])
+    return res
