@@ -1,0 +1,435 @@
+// Sparse causal attention forward for gfx950 (MI355X, CDNA4).
+//
+// Computes, for every query row i of chunk a, O_i = softmax_j(scale * q_i.k_j) v_j
+// over the keys j of {c_0, c_{a-W}, ..., c_a} (TalkingMachines, Sec. 4.2: the
+// sparse attention pattern and its attention equation). The key set of a query
+// chunk is a union of at most a few contiguous key ranges; query tiles never
+// straddle a chunk, so every row of a tile shares its ranges, key tiles are
+// visited only inside those ranges (masked blocks are never loaded), and only
+// the last key tile of a range needs a column mask.
+//
+// bf16 kernel: one workgroup of 4 waves per 128-row query tile, 32 query rows
+// per wave. Per 64-key tile:
+//   S^T (keys x queries) = K Q^T with v_mfma_f32_32x32x16_bf16, K from LDS,
+//     Q^T held in registers for the whole loop;
+//   online softmax in fp32 on the MFMA output layout, where each lane owns one
+//     query column, so the row max needs one exchange between the two
+//     half-waves and the row sum none until the end; exp2 with the scale
+//     folded in, and a lazily-updated running max (the accumulator is only
+//     rescaled when the max grows by more than 2^8, which keeps P <= 256);
+//   O^T (head_dim x queries) += V^T P^T with the same MFMA, P^T straight from
+//     registers (bf16, rounded to nearest even) and V^T fragments read from the
+//     row-major LDS V tile with the gfx950 transposing LDS read.
+// Global->LDS staging is software-pipelined through registers: the next key
+// tile's loads are in flight while the current tile is computed.
+//
+// fp32 kernel: a plain VALU kernel (4 lanes per query row, exact running max)
+// for fp32 inputs; it exists for correctness at small sizes.
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "tm_internal.h"
+
+namespace tmk {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+
+constexpr float kNegInf = -__builtin_inff();
+
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
+// Renumber them so that consecutive logical ids (the query tiles of one head,
+// which stream the same K/V) land on the same XCD.
+__device__ __forceinline__ int xcd_logical_id(int bid, int total) {
+    constexpr int kXcds = 8;
+    const int per = total / kXcds, rem = total % kXcds;
+    const int x = bid % kXcds, j = bid / kXcds;
+    return x * per + min(x, rem) + j;
+}
+
+// Query rows [q0, q1) of tile `tile` and its key ranges. Mode 0 reads the
+// ranges from the kernel arguments; mode 1 derives them from the geometry.
+struct TileRanges {
+    int q0, q1;
+    int n;         // number of ranges
+    int b0, e0;    // mode 1 ranges (at most two)
+    int b1, e1;
+};
+
+template <int BM>
+__device__ __forceinline__ TileRanges plan_tile(const AttnArgs& a, int tile) {
+    TileRanges t;
+    if (a.mode == 0) {
+        t.q0 = tile * BM;
+        t.q1 = min(t.q0 + BM, a.Lq);
+        t.n = a.n_ranges;
+        t.b0 = t.e0 = t.b1 = t.e1 = 0;
+        return t;
+    }
+    // Mode 1: tiles are ordered heaviest first (the last chunks see the most
+    // keys), so walk the natural order backwards.
+    const int nat = a.n_qtiles - 1 - tile;
+    int chunk;
+    if (nat < a.ref_tiles) {
+        chunk = 0;
+        t.q0 = nat * BM;
+        t.q1 = min(t.q0 + BM, a.ref_tok);
+    } else {
+        const int u = nat - a.ref_tiles;
+        chunk = 1 + u / a.chunk_tiles;
+        const int cs = a.ref_tok + (chunk - 1) * a.chunk_tok;
+        const int ce = min(cs + a.chunk_tok, a.seq_len);
+        t.q0 = cs + (u % a.chunk_tiles) * BM;
+        t.q1 = min(t.q0 + BM, ce);
+    }
+    if (chunk == 0) {
+        t.n = 1;
+        t.b0 = 0;
+        t.e0 = a.ref_tok;
+        t.b1 = t.e1 = 0;
+    } else {
+        const int lo = max(1, chunk - a.window);
+        const int end = min(a.ref_tok + chunk * a.chunk_tok, a.seq_len);
+        if (lo == 1) {  // c_0 and c_1 are adjacent: one range
+            t.n = 1;
+            t.b0 = 0;
+            t.e0 = end;
+            t.b1 = t.e1 = 0;
+        } else {
+            t.n = 2;
+            t.b0 = 0;
+            t.e0 = a.ref_tok;
+            t.b1 = a.ref_tok + (lo - 1) * a.chunk_tok;
+            t.e1 = end;
+        }
+    }
+    return t;
+}
+
+__device__ __forceinline__ int range_begin(const AttnArgs& a, const TileRanges& t, int r) {
+    return a.mode == 0 ? a.range_begin[r] : (r == 0 ? t.b0 : t.b1);
+}
+__device__ __forceinline__ int range_end(const AttnArgs& a, const TileRanges& t, int r) {
+    return a.mode == 0 ? a.range_end[r] : (r == 0 ? t.e0 : t.e1);
+}
+
+__device__ __forceinline__ f32x16_t mfma32x32x16(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// ----------------------------------------------------------------------------
+// bf16 MFMA kernel
+// ----------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const AttnArgs a) {
+    constexpr int BM = kTileRowsBf16;  // query rows per workgroup
+    constexpr int BN = 64;             // keys per tile
+    constexpr int KSTR = D + 8;        // LDS row pitch of K (elements)
+    constexpr int VSTR = D + 16;       // LDS row pitch of V (elements)
+    constexpr int CPR = D / 8;         // 16-byte chunks per key row
+    constexpr int LD = BN * CPR / 256; // 16-byte chunks per thread per tile
+    constexpr int KK = D / 16;         // MFMA k-steps over head_dim
+    constexpr int DB = D / 32;         // 32-row blocks of O^T
+    static_assert(BN * CPR % 256 == 0, "tile must split evenly over 256 threads");
+
+    __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KSTR];
+    __shared__ __attribute__((aligned(16))) __bf16 Vs[BN * VSTR];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int hw = lane >> 5;   // half-wave: which 8-element k-slice a lane feeds
+    const int l32 = lane & 31;  // the query column (and operand row) a lane owns
+
+    const int total = a.n_qtiles * a.B * a.H;
+    const int id = xcd_logical_id(blockIdx.x, total);
+    const int tile = id % a.n_qtiles;
+    const int bh = id / a.n_qtiles;
+    const int head = bh % a.H;
+    const int bat = bh / a.H;
+    const TileRanges tr = plan_tile<BM>(a, tile);
+
+    const __bf16* qp = static_cast<const __bf16*>(a.q) + bat * a.q_sb + head * a.q_sh;
+    const __bf16* kp = static_cast<const __bf16*>(a.k) + bat * a.k_sb + head * a.k_sh;
+    const __bf16* vp = static_cast<const __bf16*>(a.v) + bat * a.v_sb + head * a.v_sh;
+
+    // Q^T operand (B of the S^T MFMA): lane holds q[row][16*kk + 8*hw .. +8].
+    const int qrow = tr.q0 + wave * 32 + l32;
+    const bool row_ok = qrow < tr.q1;
+    bf16x8_t qf[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        if (row_ok) {
+            qf[kk] = *reinterpret_cast<const bf16x8_t*>(qp + qrow * a.q_st + kk * 16 + hw * 8);
+        } else {
+            qf[kk] = bf16x8_t{};
+        }
+    }
+
+    f32x16_t acc[DB];
+#pragma unroll
+    for (int i = 0; i < DB; ++i) acc[i] = f32x16_t{};
+    float m_run = kNegInf;  // running max in the scaled log2 domain
+    float l_run = 0.f;      // this lane's partial row sum (its 32 keys per tile)
+    const float c = a.scale_log2;
+
+    uint4 kreg[LD], vreg[LD];
+    auto load_tile = [&](int k0, int ke) {
+#pragma unroll
+        for (int i = 0; i < LD; ++i) {
+            const int ch = tid + 256 * i;
+            const int row = ch / CPR, col = ch % CPR;
+            const int key = k0 + row;
+            if (key < ke) {
+                kreg[i] = *reinterpret_cast<const uint4*>(kp + key * a.k_st + col * 8);
+                vreg[i] = *reinterpret_cast<const uint4*>(vp + key * a.v_st + col * 8);
+            } else {  // past the range end: zeros (finite, so 0 * v stays 0)
+                kreg[i] = make_uint4(0, 0, 0, 0);
+                vreg[i] = make_uint4(0, 0, 0, 0);
+            }
+        }
+    };
+    auto store_tile = [&]() {
+#pragma unroll
+        for (int i = 0; i < LD; ++i) {
+            const int ch = tid + 256 * i;
+            const int row = ch / CPR, col = ch % CPR;
+            *reinterpret_cast<uint4*>(&Ks[row * KSTR + col * 8]) = kreg[i];
+            *reinterpret_cast<uint4*>(&Vs[row * VSTR + col * 8]) = vreg[i];
+        }
+    };
+
+    int r = 0;
+    int k0 = range_begin(a, tr, 0);
+    load_tile(k0, range_end(a, tr, 0));
+    while (true) {
+        const int ke = range_end(a, tr, r);
+        __syncthreads();  // everyone is done reading the previous tile
+        store_tile();
+        __syncthreads();
+
+        // Issue the next tile's global loads; they land while this one computes.
+        int nr = r, nk0 = k0 + BN;
+        if (nk0 >= ke) {
+            nr = r + 1;
+            if (nr < tr.n) nk0 = range_begin(a, tr, nr);
+        }
+        const bool has_next = nr < tr.n;
+        if (has_next) load_tile(nk0, range_end(a, tr, nr));
+
+        // ---- S^T = K Q^T: two 32-key blocks x 32 queries per wave
+        f32x16_t s0 = f32x16_t{}, s1 = f32x16_t{};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&Ks[l32 * KSTR + kk * 16 + hw * 8]);
+            const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(&Ks[(32 + l32) * KSTR + kk * 16 + hw * 8]);
+            s0 = mfma32x32x16(ka, qf[kk], s0);
+            s1 = mfma32x32x16(kb, qf[kk], s1);
+        }
+
+        // Output layout: register i of a lane holds key row 8*(i/4) + 4*hw + i%4.
+        if (k0 + BN > ke) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int kr = k0 + 8 * (i / 4) + 4 * hw + (i % 4);
+                if (kr >= ke) s0[i] = kNegInf;
+                if (kr + 32 >= ke) s1[i] = kNegInf;
+            }
+        }
+
+        // ---- online softmax
+        float mx = s0[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx * c);
+        if (__any(m_new > m_run + 8.f)) {
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int d = 0; d < DB; ++d) acc[d] *= alpha;
+        }
+        const float neg_m = -m_run;
+        bf16x8_t pf[4];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(s0[i], c, neg_m));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(s1[i], c, neg_m));
+            l_run += p0 + p1;
+            pf[i / 8][i % 8] = static_cast<__bf16>(p0);
+            pf[2 + i / 8][i % 8] = static_cast<__bf16>(p1);
+        }
+
+        // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*(j%2) .. of block
+        // j/2 with slot e <-> row 16*(j%2) + 4*hw + e (e < 4) or
+        // 16*(j%2) + 8 + 4*hw + (e - 4) (e >= 4); the V^T operand must use the
+        // same key order, read 4 keys at a time with the transposing LDS read.
+        const int grp = lane >> 4;  // 16-lane group
+        const int gi = lane & 15;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int kb0 = 16 * j + 4 * hw;  // 16*(j%2) + 32*(j/2) == 16*j
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+                const int col = 32 * d + 16 * (grp & 1) + 4 * (gi & 3);
+                const __bf16* p0 = &Vs[(kb0 + (gi >> 2)) * VSTR + col];
+                const __bf16* p1 = &Vs[(kb0 + 8 + (gi >> 2)) * VSTR + col];
+                const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p0));
+                const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p1));
+                const bf16x8_t vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                acc[d] = mfma32x32x16(vf, pf[j], acc[d]);
+            }
+        }
+
+        if (!has_next) break;
+        r = nr;
+        k0 = nk0;
+    }
+
+    // ---- epilogue: normalise, round to bf16, store rows inside the tile
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float inv = 1.f / l_tot;
+    if (row_ok) {
+        __bf16* op = static_cast<__bf16*>(a.o) + bat * a.o_sb + head * a.o_sh + qrow * a.o_st;
+#pragma unroll
+        for (int d = 0; d < DB; ++d) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                bf16x4_t w;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[d][4 * g + e] * inv);
+                *reinterpret_cast<bf16x4_t*>(op + 32 * d + 8 * g + 4 * hw) = w;
+            }
+        }
+        if (a.lse != nullptr && hw == 0) {
+            a.lse[(static_cast<int64_t>(bat) * a.H + head) * a.Lq + qrow] =
+                (m_run + __log2f(l_tot)) * 0.69314718055994530942f;
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------
+// fp32 VALU kernel (small problems, exact fp32 arithmetic)
+// ----------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void attn_fwd_f32_kernel(const AttnArgs a) {
+    constexpr int BM = kTileRowsF32;  // 64 query rows, 4 lanes each
+    constexpr int BN = 32;
+    constexpr int DP = D / 4;         // elements per lane
+    constexpr int PSTR = DP + 1;      // padded quarter-row pitch in LDS
+    constexpr int RSTR = 4 * PSTR;
+    constexpr int C4 = D / 4;         // float4 per key row
+
+    __shared__ float Ks[BN * RSTR];
+    __shared__ float Vs[BN * RSTR];
+
+    const int tid = threadIdx.x;
+    const int row = tid >> 2, part = tid & 3;
+    const int total = a.n_qtiles * a.B * a.H;
+    const int id = xcd_logical_id(blockIdx.x, total);
+    const int tile = id % a.n_qtiles;
+    const int bh = id / a.n_qtiles;
+    const int head = bh % a.H;
+    const int bat = bh / a.H;
+    const TileRanges tr = plan_tile<BM>(a, tile);
+
+    const float* qp = static_cast<const float*>(a.q) + bat * a.q_sb + head * a.q_sh;
+    const float* kp = static_cast<const float*>(a.k) + bat * a.k_sb + head * a.k_sh;
+    const float* vp = static_cast<const float*>(a.v) + bat * a.v_sb + head * a.v_sh;
+    const int qrow = tr.q0 + row;
+    const bool row_ok = qrow < tr.q1;
+
+    float qv[DP], ov[DP];
+#pragma unroll
+    for (int e = 0; e < DP; ++e) {
+        qv[e] = row_ok ? qp[qrow * a.q_st + part * DP + e] : 0.f;
+        ov[e] = 0.f;
+    }
+    float m = kNegInf, l = 0.f;
+    const float c = a.scale_log2;
+
+    for (int r = 0; r < tr.n; ++r) {
+        const int kb = range_begin(a, tr, r), ke = range_end(a, tr, r);
+        for (int k0 = kb; k0 < ke; k0 += BN) {
+            __syncthreads();
+            for (int ch = tid; ch < BN * C4; ch += 256) {
+                const int kr = ch / C4, c4 = ch % C4;
+                float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
+                if (k0 + kr < ke) {
+                    kv = *reinterpret_cast<const float4*>(kp + (k0 + kr) * a.k_st + c4 * 4);
+                    vv = *reinterpret_cast<const float4*>(vp + (k0 + kr) * a.v_st + c4 * 4);
+                }
+                const int d0 = c4 * 4;
+                const int base = kr * RSTR + (d0 / DP) * PSTR + d0 % DP;
+                Ks[base + 0] = kv.x; Ks[base + 1] = kv.y; Ks[base + 2] = kv.z; Ks[base + 3] = kv.w;
+                Vs[base + 0] = vv.x; Vs[base + 1] = vv.y; Vs[base + 2] = vv.z; Vs[base + 3] = vv.w;
+            }
+            __syncthreads();
+            const int n = min(BN, ke - k0);
+            for (int j = 0; j < n; ++j) {
+                const float* kr = &Ks[j * RSTR + part * PSTR];
+                float dot = 0.f;
+#pragma unroll
+                for (int e = 0; e < DP; ++e) dot = fmaf(qv[e], kr[e], dot);
+                dot += __shfl_xor(dot, 1);
+                dot += __shfl_xor(dot, 2);
+                const float s = dot * c;
+                const float m_new = fmaxf(m, s);
+                const float alpha = exp2f(m - m_new);
+                const float p = exp2f(s - m_new);
+                l = fmaf(l, alpha, p);
+                const float* vr = &Vs[j * RSTR + part * PSTR];
+#pragma unroll
+                for (int e = 0; e < DP; ++e) ov[e] = fmaf(ov[e], alpha, p * vr[e]);
+                m = m_new;
+            }
+        }
+    }
+
+    if (row_ok) {
+        float* op = static_cast<float*>(a.o) + bat * a.o_sb + head * a.o_sh + qrow * a.o_st;
+        const float inv = 1.f / l;
+#pragma unroll
+        for (int e = 0; e < DP; ++e) op[part * DP + e] = ov[e] * inv;
+        if (a.lse != nullptr && part == 0) {
+            a.lse[(static_cast<int64_t>(bat) * a.H + head) * a.Lq + qrow] =
+                (m + log2f(l)) * 0.69314718055994530942f;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
+    const dim3 grid(a.n_qtiles * a.B * a.H), block(256);
+    if (head_dim == 128) {
+        hipLaunchKernelGGL(attn_fwd_bf16_kernel<128>, grid, block, 0, s, a);
+    } else if (head_dim == 64) {
+        hipLaunchKernelGGL(attn_fwd_bf16_kernel<64>, grid, block, 0, s, a);
+    } else {
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t s) {
+    const dim3 grid(a.n_qtiles * a.B * a.H), block(256);
+    if (head_dim == 128) {
+        hipLaunchKernelGGL(attn_fwd_f32_kernel<128>, grid, block, 0, s, a);
+    } else if (head_dim == 64) {
+        hipLaunchKernelGGL(attn_fwd_f32_kernel<64>, grid, block, 0, s, a);
+    } else {
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace tmk

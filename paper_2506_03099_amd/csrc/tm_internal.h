@@ -1,0 +1,57 @@
+// Internal interface between the host-side API (tm_api.cpp) and the HIP
+// kernels (attn_fwd.hip, kv_append.hip). Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tmk {
+
+constexpr int kMaxRanges = 16;  // key ranges of one query segment (>= TM_MAX_WINDOW + 2)
+
+// Rows per query tile of each attention kernel; the host needs them to count
+// tiles per chunk.
+constexpr int kTileRowsBf16 = 128;
+constexpr int kTileRowsF32 = 64;
+
+// One attention launch. Element strides (not bytes) for batch, token and head.
+struct AttnArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    float* lse;  // [B, H, Lq] or null
+    int64_t q_sb, q_st, q_sh;
+    int64_t k_sb, k_st, k_sh;
+    int64_t v_sb, v_st, v_sh;
+    int64_t o_sb, o_st, o_sh;
+    int32_t B, H, Lq;
+    float scale_log2;  // softmax scale * log2(e)
+    int32_t n_qtiles;  // query tiles per (batch, head)
+    // mode 0: every query row of the buffer belongs to one chunk and sees the
+    //         same key ranges (streaming form, or one chunk of a sequence);
+    // mode 1: the buffer holds a whole sequence (row i = position i); each
+    //         tile's chunk and key ranges follow from the geometry below.
+    int32_t mode;
+    int32_t n_ranges;  // mode 0
+    int32_t range_begin[kMaxRanges];
+    int32_t range_end[kMaxRanges];
+    int32_t ref_tok;      // mode 1: R*T (clipped to the sequence)
+    int32_t chunk_tok;    // mode 1: C*T
+    int32_t window;       // mode 1: W
+    int32_t seq_len;      // mode 1: tokens in the sequence
+    int32_t ref_tiles;    // mode 1: query tiles of c_0
+    int32_t chunk_tiles;  // mode 1: query tiles of a full chunk
+};
+
+hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t s);
+
+// Copy n_tok tokens of K and V from [B, n_tok, H, D] into pools laid out
+// [B, H, capacity, D] at token row `tok_offset`. `row_bytes` = D * element
+// size (a multiple of 16).
+hipError_t launch_kv_append(const void* k_src, const void* v_src, void* k_pool, void* v_pool,
+                            int B, int n_tok, int H, int row_bytes, int64_t capacity,
+                            int64_t tok_offset, hipStream_t s);
+
+}  // namespace tmk

@@ -1,0 +1,139 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+The library must load and export every function ``include/tm.h`` declares;
+argument validation must reject bad input on the host, before any launch,
+with the documented status; the key-range planner's pair counts must equal
+the oracle's mask counts.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import ChunkGeometry, allowed_mask
+from oracle.attention import chunk_start
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tm.h")
+
+
+@pytest.fixture(scope="module")
+def tm():
+    from paper_2506_03099_amd import tm as binding
+    return binding
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tm_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function(tm):
+    names = _declared_functions()
+    assert "tm_kv_append" in names and "tm_sparse_causal_attn_fwd" in names
+    lib = tm.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _desc(tm, **kw):
+    base = dict(batch=1, heads=40, head_dim=128, tokens_per_frame=1560, chunk_frames=3,
+                ref_frames=1, window=1, dtype=tm.TM_BF16, softmax_scale=0.0)
+    base.update(kw)
+    return tm.tm_attn_desc(**base)
+
+
+def test_cache_size_arithmetic(tm):
+    d = _desc(tm)
+    assert tm.tm_kv_cache_tokens(d) == 1560 + 2 * 4680 == 10920
+    assert tm.tm_kv_cache_bytes(d) == 40 * 10920 * 128 * 2
+    d2 = _desc(tm, batch=2, tokens_per_frame=3600, dtype=tm.TM_F32, window=3)
+    assert tm.tm_kv_cache_tokens(d2) == 3600 + 4 * 10800
+    assert tm.tm_kv_cache_bytes(d2) == 2 * 40 * (3600 + 4 * 10800) * 128 * 4
+
+
+@pytest.mark.parametrize("kw", [dict(head_dim=96), dict(head_dim=0), dict(batch=0),
+                                dict(heads=0), dict(tokens_per_frame=0), dict(chunk_frames=0),
+                                dict(ref_frames=0), dict(window=-1), dict(window=13),
+                                dict(dtype=7)])
+def test_invalid_descriptor_has_no_cache_size(tm, kw):
+    assert tm.tm_kv_cache_bytes(_desc(tm, **kw)) == 0
+    assert tm.tm_kv_cache_tokens(_desc(tm, **kw)) == 0
+
+
+FAKE = 1 << 40  # aligned, non-null, but not device memory
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), -2), (dict(dtype=5), -3), (dict(window=13), -2),
+    (dict(softmax_scale=float("nan")), -1), (dict(softmax_scale=float("inf")), -1),
+])
+def test_forward_rejects_bad_descriptor(tm, kw, status):
+    d = _desc(tm, **kw)
+    st = tm.lib().tm_sparse_causal_attn_fwd(ctypes.byref(d), FAKE, -1, None, FAKE, FAKE, 21,
+                                            FAKE, None, None)
+    assert st == status
+    assert tm.tm_last_error() != ""
+
+
+def test_forward_rejects_bad_sequence_arguments(tm):
+    d = _desc(tm)
+    L = tm.lib()
+    call = lambda qc, nf, q=FAKE, k=FAKE, v=FAKE, o=FAKE: L.tm_sparse_causal_attn_fwd(
+        ctypes.byref(d), q, qc, None, k, v, nf, o, None, None)
+    assert call(-1, 0) == tm.TM_E_SHAPE           # no frames
+    assert call(8, 21) == tm.TM_E_SHAPE           # only chunks 0..7 exist
+    assert call(-2, 21) == tm.TM_E_SHAPE
+    assert call(-1, 21, q=None) == tm.TM_E_ARG     # NULL pointer
+    assert call(-1, 21, k=FAKE + 8) == tm.TM_E_ARG  # misaligned
+    assert call(-1, 21) == tm.TM_E_ARG             # not device memory
+
+
+def test_append_and_cache_reject_bad_arguments(tm):
+    L = tm.lib()
+    d = _desc(tm)
+    assert L.tm_kv_append(None, 0, FAKE, FAKE, 10, None) == tm.TM_E_ARG
+    h = ctypes.c_void_p()
+    assert L.tm_kv_cache_create(ctypes.byref(d), FAKE, FAKE, ctypes.byref(h)) == tm.TM_E_ARG
+    assert L.tm_kv_cache_create(ctypes.byref(d), FAKE, FAKE + (1 << 32), ctypes.byref(h)) == tm.TM_E_ARG
+    assert h.value is None
+    assert L.tm_kv_cache_create(None, FAKE, FAKE, ctypes.byref(h)) == tm.TM_E_ARG
+    assert L.tm_kv_cache_reset(None) == tm.TM_E_ARG
+    assert L.tm_kv_cache_latest(None) == -1
+
+
+def _oracle_pairs(n_frames, T, C, R, W, q_chunk):
+    g = ChunkGeometry(T, C, R, W)
+    L = n_frames * T
+    pos = np.arange(L)
+    if q_chunk >= 0:
+        lo = chunk_start(q_chunk, g)
+        hi = min(chunk_start(q_chunk + 1, g), L)
+        qpos = pos[lo:hi]
+    else:
+        qpos = pos
+    return int(allowed_mask(qpos, pos, g).sum())
+
+
+@pytest.mark.parametrize("n_frames,T,C,R,W", [
+    (21, 1560, 3, 1, 1), (21, 1560, 3, 3, 1), (9, 64, 2, 1, 1), (13, 7, 2, 1, 0),
+    (13, 7, 2, 2, 3), (5, 11, 4, 1, 1), (2, 5, 3, 3, 1), (30, 3, 1, 1, 12),
+])
+def test_planner_pair_counts_equal_oracle_mask_counts(tm, n_frames, T, C, R, W):
+    d = _desc(tm, heads=1, tokens_per_frame=T, chunk_frames=C, ref_frames=R, window=W)
+    L = n_frames * T
+    n_chunks = 1 if L <= R * T else 1 + -(-(L - R * T) // (C * T))
+    if L <= 3000:
+        assert tm.tm_allowed_pairs(d, -1, None, n_frames) == _oracle_pairs(n_frames, T, C, R, W, -1)
+    for a in range(n_chunks):
+        if L <= 3000 or a in (0, 1, n_chunks - 1):
+            assert tm.tm_allowed_pairs(d, a, None, n_frames) == _oracle_pairs(n_frames, T, C, R, W, a)
+    assert tm.tm_allowed_pairs(d, n_chunks, None, n_frames) == -1
+
+
+def test_planner_full_sequence_480p_total(tm):
+    d = _desc(tm)
+    assert tm.tm_allowed_pairs(d, -1, None, 21) == 316_368_000
