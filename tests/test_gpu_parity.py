@@ -390,7 +390,14 @@ def test_480p_full_sequence_sampled(tm):
     heads = [3, 29]
     say(f"480p full sequence: heads {heads}, {len(rows)} rows")
     o_ref, _ = full_sequence_attention(d["q"], d["k"], d["v"], g, heads=heads, rows=rows)
-    assert_close(from_dev(o)[:, rows][:, :, heads], o_ref, "bf16", "480p full sequence")
+    got = from_dev(o)[:, rows][:, :, heads]
+    # Each query chunk is its own attention problem (c_0 rows see 1560 keys,
+    # later rows up to 10920, so output scales differ by ~2.6x): the bar
+    # applies to each chunk's rows with that chunk's RMS.
+    chunk_of_row = np.searchsorted(np.array(bounds[1:]), rows, side="right")
+    for a in np.unique(chunk_of_row):
+        sel = chunk_of_row == a
+        assert_close(got[:, sel], o_ref[:, sel], "bf16", f"480p full sequence chunk {a}")
 
 
 def test_720p_two_streams_sampled(tm):
