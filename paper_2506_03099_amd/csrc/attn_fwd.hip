@@ -125,20 +125,42 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(bf16x8_t a, bf16x8_t b, f32x16_
 // ----------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ----------------------------------------------------------------------------
+// LDS holds two K tiles and two V tiles (double buffering), each BN rows of D
+// bf16 with no padding. Every 16-byte chunk of a row sits at chunk position
+// (chunk ^ swz(row)), which spreads both the K operand reads (same chunk of
+// consecutive rows) and the transposing V reads (two adjacent chunks of four
+// consecutive rows) over distinct banks. Tiles are filled by direct
+// global->LDS loads (global_load_lds_dwordx4): each wave instruction writes
+// 1 KB of LDS linearly, so each lane fetches the global chunk that belongs at
+// its LDS position.
 template <int D>
-__global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const AttnArgs a) {
+__device__ __forceinline__ int lds_swizzle(int row) {
+    constexpr int half = D / 16;  // chunks per row / 2
+    return 2 * (row & (half - 1)) + ((row / half) & 1);
+}
+
+template <int D>
+struct Bf16Smem {
+    static constexpr int kTileBytes = 64 * D * 2;
+    __attribute__((aligned(1024))) unsigned char k0[kTileBytes];
+    __attribute__((aligned(1024))) unsigned char k1[kTileBytes];
+    __attribute__((aligned(1024))) unsigned char v0[kTileBytes];
+    __attribute__((aligned(1024))) unsigned char v1[kTileBytes];
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(const AttnArgs a) {
     constexpr int BM = kTileRowsBf16;  // query rows per workgroup
     constexpr int BN = 64;             // keys per tile
-    constexpr int KSTR = D + 8;        // LDS row pitch of K (elements)
-    constexpr int VSTR = D + 16;       // LDS row pitch of V (elements)
     constexpr int CPR = D / 8;         // 16-byte chunks per key row
-    constexpr int LD = BN * CPR / 256; // 16-byte chunks per thread per tile
-    constexpr int KK = D / 16;         // MFMA k-steps over head_dim
-    constexpr int DB = D / 32;         // 32-row blocks of O^T
-    static_assert(BN * CPR % 256 == 0, "tile must split evenly over 256 threads");
+    constexpr int ROWB = D * 2;        // bytes per key row
+    constexpr int TILEB = BN * ROWB;
+    constexpr int NI = TILEB / (256 * 16);  // direct loads per thread per tensor per tile
+    constexpr int KK = D / 16;              // MFMA k-steps over head_dim
+    constexpr int DB = D / 32;              // 32-row blocks of O^T
+    static_assert(NI * 256 * 16 == TILEB, "tile must split evenly over 256 threads");
 
-    __shared__ __attribute__((aligned(16))) __bf16 Ks[BN * KSTR];
-    __shared__ __attribute__((aligned(16))) __bf16 Vs[BN * VSTR];
+    __shared__ Bf16Smem<D> sm;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -157,6 +179,25 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const AttnArgs a) {
     const __bf16* qp = static_cast<const __bf16*>(a.q) + bat * a.q_sb + head * a.q_sh;
     const __bf16* kp = static_cast<const __bf16*>(a.k) + bat * a.k_sb + head * a.k_sh;
     const __bf16* vp = static_cast<const __bf16*>(a.v) + bat * a.v_sb + head * a.v_sh;
+
+    // Issue the direct loads of one K tile and one V tile. Rows past the range
+    // end re-read the range's last row (finite data; its scores are masked).
+    auto issue = [&](int k0, int ke, unsigned char* kd, unsigned char* vd) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int blk = i * 4 + wave;  // 1 KB block of the tile
+            const int ch = blk * 64 + lane;
+            const int row = ch / CPR;
+            const int gc = (ch % CPR) ^ lds_swizzle<D>(row);
+            const int key = min(k0 + row, ke - 1);
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(kp + key * a.k_st + gc * 8),
+                (__attribute__((address_space(3))) void*)(kd + blk * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(vp + key * a.v_st + gc * 8),
+                (__attribute__((address_space(3))) void*)(vd + blk * 1024), 16, 0, 0);
+        }
+    };
 
     // Q^T operand (B of the S^T MFMA): lane holds q[row][16*kk + 8*hw .. +8].
     const int qrow = tr.q0 + wave * 32 + l32;
@@ -178,58 +219,27 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const AttnArgs a) {
     float l_run = 0.f;      // this lane's partial row sum (its 32 keys per tile)
     const float c = a.scale_log2;
 
-    uint4 kreg[LD], vreg[LD];
-    auto load_tile = [&](int k0, int ke) {
-#pragma unroll
-        for (int i = 0; i < LD; ++i) {
-            const int ch = tid + 256 * i;
-            const int row = ch / CPR, col = ch % CPR;
-            const int key = k0 + row;
-            if (key < ke) {
-                kreg[i] = *reinterpret_cast<const uint4*>(kp + key * a.k_st + col * 8);
-                vreg[i] = *reinterpret_cast<const uint4*>(vp + key * a.v_st + col * 8);
-            } else {  // past the range end: zeros (finite, so 0 * v stays 0)
-                kreg[i] = make_uint4(0, 0, 0, 0);
-                vreg[i] = make_uint4(0, 0, 0, 0);
-            }
-        }
-    };
-    auto store_tile = [&]() {
-#pragma unroll
-        for (int i = 0; i < LD; ++i) {
-            const int ch = tid + 256 * i;
-            const int row = ch / CPR, col = ch % CPR;
-            *reinterpret_cast<uint4*>(&Ks[row * KSTR + col * 8]) = kreg[i];
-            *reinterpret_cast<uint4*>(&Vs[row * VSTR + col * 8]) = vreg[i];
-        }
-    };
+    // Per-lane LDS byte offsets. K operand: row l32 (and l32 + 32), chunk
+    // 2*kk + hw. V^T operand via the transposing read: rows 16*j + 4*hw + gi/4
+    // (and + 8), element columns 32*d + 16*(grp & 1) + 4*(gi & 3).
+    const int k_row_off = l32 * ROWB;
+    const int k_swz = lds_swizzle<D>(l32);
+    const int grp = lane >> 4, gi = lane & 15;
+    const int v_row = 4 * hw + (gi >> 2);
+    const int v_swz_lo = lds_swizzle<D>(v_row), v_swz_hi = lds_swizzle<D>(v_row + 8);
+    const int v_cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
+    const int v_half = (gi & 1) * 8;
 
-    int r = 0;
-    int k0 = range_begin(a, tr, 0);
-    load_tile(k0, range_end(a, tr, 0));
-    while (true) {
-        const int ke = range_end(a, tr, r);
-        __syncthreads();  // everyone is done reading the previous tile
-        store_tile();
-        __syncthreads();
-
-        // Issue the next tile's global loads; they land while this one computes.
-        int nr = r, nk0 = k0 + BN;
-        if (nk0 >= ke) {
-            nr = r + 1;
-            if (nr < tr.n) nk0 = range_begin(a, tr, nr);
-        }
-        const bool has_next = nr < tr.n;
-        if (has_next) load_tile(nk0, range_end(a, tr, nr));
-
+    auto compute = [&](const unsigned char* kb, const unsigned char* vb, int k0, int ke) {
         // ---- S^T = K Q^T: two 32-key blocks x 32 queries per wave
         f32x16_t s0 = f32x16_t{}, s1 = f32x16_t{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(&Ks[l32 * KSTR + kk * 16 + hw * 8]);
-            const bf16x8_t kb = *reinterpret_cast<const bf16x8_t*>(&Ks[(32 + l32) * KSTR + kk * 16 + hw * 8]);
+            const int off = k_row_off + (((2 * kk + hw) ^ k_swz) << 4);
+            const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kb + off);
+            const bf16x8_t kb2 = *reinterpret_cast<const bf16x8_t*>(kb + off + 32 * ROWB);
             s0 = mfma32x32x16(ka, qf[kk], s0);
-            s1 = mfma32x32x16(kb, qf[kk], s1);
+            s1 = mfma32x32x16(kb2, qf[kk], s1);
         }
 
         // Output layout: register i of a lane holds key row 8*(i/4) + 4*hw + i%4.
@@ -268,30 +278,56 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16_kernel(const AttnArgs a) {
             pf[2 + i / 8][i % 8] = static_cast<__bf16>(p1);
         }
 
-        // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*(j%2) .. of block
-        // j/2 with slot e <-> row 16*(j%2) + 4*hw + e (e < 4) or
-        // 16*(j%2) + 8 + 4*hw + (e - 4) (e >= 4); the V^T operand must use the
-        // same key order, read 4 keys at a time with the transposing LDS read.
-        const int grp = lane >> 4;  // 16-lane group
-        const int gi = lane & 15;
+        // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*j .. 16*j + 15
+        // with slot e <-> row 16*j + 4*hw + e (e < 4) or 16*j + 8 + 4*hw + e - 4
+        // (e >= 4); the V^T operand reads the same keys, 4 at a time.
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int kb0 = 16 * j + 4 * hw;  // 16*(j%2) + 32*(j/2) == 16*j
 #pragma unroll
             for (int d = 0; d < DB; ++d) {
-                const int col = 32 * d + 16 * (grp & 1) + 4 * (gi & 3);
-                const __bf16* p0 = &Vs[(kb0 + (gi >> 2)) * VSTR + col];
-                const __bf16* p1 = &Vs[(kb0 + 8 + (gi >> 2)) * VSTR + col];
-                const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p0));
-                const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p1));
-                const bf16x8_t vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                const int cc = 4 * d + v_cbase;
+                const int lo = (16 * j + v_row) * ROWB + ((cc ^ v_swz_lo) << 4) + v_half;
+                const int hi = (16 * j + v_row + 8) * ROWB + ((cc ^ v_swz_hi) << 4) + v_half;
+                const bf16x4_t vlo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(vb + lo));
+                const bf16x4_t vhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(vb + hi));
+                const bf16x8_t vf = __builtin_shufflevector(vlo, vhi, 0, 1, 2, 3, 4, 5, 6, 7);
                 acc[d] = mfma32x32x16(vf, pf[j], acc[d]);
             }
         }
+    };
 
-        if (!has_next) break;
-        r = nr;
-        k0 = nk0;
+    // Double-buffered main loop, unrolled by two so each buffer is named
+    // statically: the loads of tile t+1 are in flight while tile t computes.
+    int r = 0;
+    int k0 = range_begin(a, tr, 0);
+    int ke = range_end(a, tr, 0);
+    issue(k0, ke, sm.k0, sm.v0);
+    auto advance = [&](int& rr, int& kk0, int& kke) -> bool {
+        kk0 += BN;
+        if (kk0 >= kke) {
+            ++rr;
+            if (rr >= tr.n) return false;
+            kk0 = range_begin(a, tr, rr);
+            kke = range_end(a, tr, rr);
+        }
+        return true;
+    };
+    while (true) {
+        int r1 = r, k1 = k0, e1 = ke;
+        bool more = advance(r1, k1, e1);
+        __syncthreads();  // tile in buffer 0 has landed; buffer 1 is free
+        if (more) issue(k1, e1, sm.k1, sm.v1);
+        compute(sm.k0, sm.v0, k0, ke);
+        if (!more) break;
+        r = r1; k0 = k1; ke = e1;
+
+        r1 = r; k1 = k0; e1 = ke;
+        more = advance(r1, k1, e1);
+        __syncthreads();  // tile in buffer 1 has landed; buffer 0 is free
+        if (more) issue(k1, e1, sm.k0, sm.v0);
+        compute(sm.k1, sm.v1, k0, ke);
+        if (!more) break;
+        r = r1; k0 = k1; ke = e1;
     }
 
     // ---- epilogue: normalise, round to bf16, store rows inside the tile
