@@ -37,6 +37,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 
@@ -135,8 +136,13 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(bf16x8_t a, bf16x8_t b, f32x16_
 // its LDS position.
 template <int D>
 __device__ __forceinline__ int lds_swizzle(int row) {
-    constexpr int half = D / 16;  // chunks per row / 2
-    return 2 * (row & (half - 1)) + ((row / half) & 1);
+    // Low three bits: a permutation of 0..7 over any 8 aligned rows (K reads
+    // of one chunk from 8 consecutive rows hit 8 distinct 16-byte bank
+    // groups), with bits 1-2 distinct over any 4 aligned rows (the V reads'
+    // chunk pairs {p, p^1} of 4 consecutive rows are disjoint). Bit 3 (rows
+    // of 16 chunks only) separates rows r and r + 8.
+    const int low = 2 * (row & 3) + ((row >> 2) & 1);
+    return D == 128 ? low + 8 * ((row >> 3) & 1) : low;
 }
 
 template <int D>
@@ -252,15 +258,22 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(const AttnArgs a)
             }
         }
 
-        // ---- online softmax
+        // ---- online softmax. The running max m_run is shared by the two
+        // half-waves holding a query's scores. It is only raised (and the
+        // accumulator rescaled) when some score exceeds it by more than 2^8,
+        // which each lane can tell from its own 32 scores; only then are the
+        // two halves' maxima combined, so the common path has no cross-lane
+        // step and m_run stays identical in both halves.
         float mx = s0[0];
 #pragma unroll
         for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx * c);
-        if (__any(m_new > m_run + 8.f)) {
+        if (__any(mx * c > m_run + 8.f)) {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx),
+                                                             __float_as_uint(mx), false, false);
+            mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // both halves
+            const float m_new = fmaxf(m_run, mx * c);
             const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
@@ -271,11 +284,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(const AttnArgs a)
         bf16x8_t pf[4];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const float p0 = __builtin_amdgcn_exp2f(fmaf(s0[i], c, neg_m));
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(s1[i], c, neg_m));
-            l_run += p0 + p1;
-            pf[i / 8][i % 8] = static_cast<__bf16>(p0);
-            pf[2 + i / 8][i % 8] = static_cast<__bf16>(p1);
+            pf[i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s0[i], c, neg_m)));
+            pf[2 + i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s1[i], c, neg_m)));
+        }
+        // Row sum of the bf16-rounded P that is multiplied into V, two at a time.
+        const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bf16x2_t pp = {pf[j][2 * e], pf[j][2 * e + 1]};
+                l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l_run, false);
+            }
         }
 
         // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*j .. 16*j + 15
