@@ -8,20 +8,20 @@
 // visited only inside those ranges (masked blocks are never loaded), and only
 // the last key tile of a range needs a column mask.
 //
-// bf16 kernel: one workgroup of 4 waves per 128-row query tile, 32 query rows
-// per wave. Per 64-key tile:
+// bf16 kernel: one workgroup of 8 waves (two per SIMD) per 256-row query tile,
+// 32 query rows per wave; all 8 waves share each K/V tile staged in LDS.
+// Per 64-key tile:
 //   S^T (keys x queries) = K Q^T with v_mfma_f32_32x32x16_bf16, K from LDS,
 //     Q^T held in registers for the whole loop;
 //   online softmax in fp32 on the MFMA output layout, where each lane owns one
-//     query column, so the row max needs one exchange between the two
-//     half-waves and the row sum none until the end; exp2 with the scale
-//     folded in, and a lazily-updated running max (the accumulator is only
-//     rescaled when the max grows by more than 2^8, which keeps P <= 256);
+//     query column and half of its keys; exp2 with the scale folded in, and a
+//     lazily-updated running max (the accumulator is only rescaled when the
+//     max grows by more than 2^8, which keeps P <= 256);
 //   O^T (head_dim x queries) += V^T P^T with the same MFMA, P^T straight from
 //     registers (bf16, rounded to nearest even) and V^T fragments read from the
 //     row-major LDS V tile with the gfx950 transposing LDS read.
-// Global->LDS staging is software-pipelined through registers: the next key
-// tile's loads are in flight while the current tile is computed.
+// K/V tiles are double-buffered in LDS and filled by direct global->LDS loads,
+// so the next tile's loads are in flight while the current tile is computed.
 //
 // fp32 kernel: a plain VALU kernel (4 lanes per query row, exact running max)
 // for fp32 inputs; it exists for correctness at small sizes.
@@ -42,6 +42,9 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 
 constexpr float kNegInf = -__builtin_inff();
+// Threads per workgroup of the bf16 kernel: 8 waves (two per SIMD) sharing
+// every K/V tile staged in LDS.
+constexpr int kBf16Threads = 512;
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
 // Renumber them so that consecutive logical ids (the query tiles of one head,
@@ -155,16 +158,18 @@ struct Bf16Smem {
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(const AttnArgs a) {
+__global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const AttnArgs a) {
     constexpr int BM = kTileRowsBf16;  // query rows per workgroup
     constexpr int BN = 64;             // keys per tile
     constexpr int CPR = D / 8;         // 16-byte chunks per key row
     constexpr int ROWB = D * 2;        // bytes per key row
     constexpr int TILEB = BN * ROWB;
-    constexpr int NI = TILEB / (256 * 16);  // direct loads per thread per tensor per tile
+    constexpr int NW = kBf16Threads / 64;   // waves per workgroup, 32 query rows each
+    constexpr int NI = TILEB / (kBf16Threads * 16);  // direct loads per thread per tensor per tile
     constexpr int KK = D / 16;              // MFMA k-steps over head_dim
     constexpr int DB = D / 32;              // 32-row blocks of O^T
-    static_assert(NI * 256 * 16 == TILEB, "tile must split evenly over 256 threads");
+    static_assert(NI * kBf16Threads * 16 == TILEB, "tile must split evenly over the threads");
+    static_assert(BM == NW * 32, "one 32-row query block per wave");
 
     __shared__ Bf16Smem<D> sm;
 
@@ -191,7 +196,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_bf16_kernel(const AttnArgs a)
     auto issue = [&](int k0, int ke, unsigned char* kd, unsigned char* vd) {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
-            const int blk = i * 4 + wave;  // 1 KB block of the tile
+            const int blk = i * NW + wave;  // 1 KB block of the tile
             const int ch = blk * 64 + lane;
             const int row = ch / CPR;
             const int gc = (ch % CPR) ^ lds_swizzle<D>(row);
@@ -465,7 +470,7 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(const AttnArgs a) {
 }  // namespace
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-    const dim3 grid(a.n_qtiles * a.B * a.H), block(256);
+    const dim3 grid(a.n_qtiles * a.B * a.H), block(kBf16Threads);
     if (head_dim == 128) {
         hipLaunchKernelGGL(attn_fwd_bf16_kernel<128>, grid, block, 0, s, a);
     } else if (head_dim == 64) {

@@ -11,7 +11,7 @@ constexpr int kMaxRanges = 16;  // key ranges of one query segment (>= TM_MAX_WI
 
 // Rows per query tile of each attention kernel; the host needs them to count
 // tiles per chunk.
-constexpr int kTileRowsBf16 = 128;
+constexpr int kTileRowsBf16 = 256;
 constexpr int kTileRowsF32 = 64;
 
 // One attention launch. Element strides (not bytes) for batch, token and head.
