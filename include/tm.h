@@ -74,15 +74,22 @@ typedef struct tm_attn_desc {
  * caller-owned pools, latest chunk index, valid length of each slot). */
 typedef struct tm_kv_cache tm_kv_cache;
 
-/* Capacity of one cache in tokens: R*T + (W+1)*C*T (c_0 plus a ring of W+1
- * chunk slots), or 0 if the descriptor is invalid. */
+/* Capacity of one cache in token rows per (batch, head), or 0 if the
+ * descriptor is invalid. c_0 is given RC = R*T rounded up to a multiple of 8
+ * rows, each of the W+1 ring slots CC = C*T rounded up to a multiple of 8, and
+ * the total RC + (W+1)*CC is rounded up to a multiple of 64 (the V pool's
+ * block). */
 int64_t tm_kv_cache_tokens(const tm_attn_desc* desc);
 
 /* Bytes of ONE pool (the K pool or the V pool) of one cache:
  * B * H * tm_kv_cache_tokens(desc) * D * sizeof(dtype), or 0 if invalid.
- * Pool layout: [B, H, capacity, D], i.e. each head's cached keys are one
- * contiguous run of D-element rows; c_0 occupies token rows [0, R*T) and ring
- * slot s occupies rows [R*T + s*C*T, R*T + (s+1)*C*T). */
+ * c_0 occupies token rows [0, R*T) and ring slot s rows [RC + s*CC, ...).
+ * K pool layout: [B, H, capacity, D], i.e. each head's cached keys are one
+ * contiguous run of D-element rows.
+ * V pool layout: [B, H, capacity/64, D, 64]: token rows in blocks of 64, each
+ * block stored dimension-major (element (row t, dim d) of a head at
+ * (t/64)*64*D + d*64 + t%64), so that 8 consecutive keys of one dimension are
+ * 16 contiguous bytes (the attention kernel's V^T operand). */
 size_t tm_kv_cache_bytes(const tm_attn_desc* desc);
 
 /* Create a cache over caller-allocated device pools of tm_kv_cache_bytes()
@@ -118,7 +125,10 @@ int32_t tm_kv_cache_latest(const tm_kv_cache* cache);
  * denoising step's when one cache is shared by the steps) or latest + 1
  * (advance). Otherwise TM_E_ORDER. n_tok in [1, R*T] for chunk 0 and
  * [1, C*T] for later chunks, else TM_E_CAPACITY. The bit patterns are copied
- * exactly. Bookkeeping is updated only when the launch succeeded. */
+ * exactly; in the V pool the rows from n_tok up to the next multiple of 8 of
+ * the chunk's region are set to zero (they are read, and masked, by the
+ * attention kernel's 8-key groups). Bookkeeping is updated only when the
+ * launch succeeded. */
 tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const void* v,
                        int32_t n_tok, hipStream_t stream);
 

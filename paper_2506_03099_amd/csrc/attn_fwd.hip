@@ -18,8 +18,12 @@
 //     lazily-updated running max (the accumulator is only rescaled when the
 //     max grows by more than 2^8, which keeps P <= 256);
 //   O^T (head_dim x queries) += V^T P^T with the same MFMA, P^T straight from
-//     registers (bf16, rounded to nearest even) and V^T fragments read from the
-//     row-major LDS V tile with the gfx950 transposing LDS read.
+//     registers (bf16, rounded to nearest even). From the KV cache, whose V
+//     blocks are stored dimension-major, the V tile lands in LDS as V^T and
+//     each operand is one 16-byte read; the K rows are fed to the S MFMA in a
+//     permuted order that makes each lane's P^T elements 8 consecutive keys.
+//     From row-major V (whole-sequence calls on caller tensors) the operand is
+//     read with the gfx950 transposing LDS read.
 // K/V tiles are double-buffered in LDS and filled by direct global->LDS loads,
 // so the next tile's loads are in flight while the current tile is computed.
 //
@@ -45,6 +49,14 @@ constexpr float kNegInf = -__builtin_inff();
 // Threads per workgroup of the bf16 kernel: 8 waves (two per SIMD) sharing
 // every K/V tile staged in LDS.
 constexpr int kBf16Threads = 512;
+// s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+// Wait until every direct global->LDS load issued by this wave has written
+// LDS. The barrier that publishes a tile only orders LDS operations; the
+// direct loads count as vector-memory operations, so each wave waits for its
+// own before the barrier, and after the barrier the whole tile is in place.
+__device__ __forceinline__ void wait_lds_dma() { __builtin_amdgcn_s_waitcnt(kWaitVmcnt0); }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
 // Renumber them so that consecutive logical ids (the query tiles of one head,
@@ -148,6 +160,18 @@ __device__ __forceinline__ int lds_swizzle(int row) {
     return D == 128 ? low + 8 * ((row >> 3) & 1) : low;
 }
 
+// V^T tile: D rows of 64 keys (128 bytes, 8 chunks of 8 keys). Chunk c of row
+// d sits at position c ^ vt_swizzle(d): over any 16 consecutive rows the pair
+// (row parity, position) takes all 16 values, so 16 lanes reading the same
+// chunk of 16 consecutive rows hit 64 distinct banks.
+__device__ __forceinline__ int vt_swizzle(int d) { return (d >> 1) & 7; }
+
+// Row of the K tile that feeds S^T row r when V is read as V^T: bits 2 and 3
+// of r swapped. The S^T output register i of a lane in half-wave hw then holds
+// key 16*(i/8) + 8*hw + i%8 of its 32-key block, so the 8 P^T elements a lane
+// feeds to a 16-key MFMA step are 8 consecutive keys.
+__device__ __forceinline__ int k_perm(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
 template <int D>
 struct Bf16Smem {
     static constexpr int kTileBytes = 64 * D * 2;
@@ -157,7 +181,7 @@ struct Bf16Smem {
     __attribute__((aligned(1024))) unsigned char v1[kTileBytes];
 };
 
-template <int D>
+template <int D, bool VT>
 __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const AttnArgs a) {
     constexpr int BM = kTileRowsBf16;  // query rows per workgroup
     constexpr int BN = 64;             // keys per tile
@@ -193,6 +217,9 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
 
     // Issue the direct loads of one K tile and one V tile. Rows past the range
     // end re-read the range's last row (finite data; its scores are masked).
+    // A V^T tile takes, for each dimension d, the 8-key groups of the tile from
+    // the cache's V block(s); groups past the range end re-read the group that
+    // holds the range's last key (its other columns are the append's zeros).
     auto issue = [&](int k0, int ke, unsigned char* kd, unsigned char* vd) {
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
@@ -204,9 +231,17 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             __builtin_amdgcn_global_load_lds(
                 (const __attribute__((address_space(1))) void*)(kp + key * a.k_st + gc * 8),
                 (__attribute__((address_space(3))) void*)(kd + blk * 1024), 16, 0, 0);
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(vp + key * a.v_st + gc * 8),
-                (__attribute__((address_space(3))) void*)(vd + blk * 1024), 16, 0, 0);
+            const __bf16* vsrc;
+            if constexpr (VT) {
+                const int d = ch >> 3;
+                const int g = min(k0 + 8 * ((ch & 7) ^ vt_swizzle(d)), (ke - 1) & ~7);
+                vsrc = vp + (g >> 6) * (64 * D) + d * 64 + (g & 63);
+            } else {
+                vsrc = vp + key * a.v_st + gc * 8;
+            }
+            __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)vsrc,
+                                             (__attribute__((address_space(3))) void*)(vd + blk * 1024),
+                                             16, 0, 0);
         }
     };
 
@@ -233,13 +268,18 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     // Per-lane LDS byte offsets. K operand: row l32 (and l32 + 32), chunk
     // 2*kk + hw. V^T operand via the transposing read: rows 16*j + 4*hw + gi/4
     // (and + 8), element columns 32*d + 16*(grp & 1) + 4*(gi & 3).
-    const int k_row_off = l32 * ROWB;
-    const int k_swz = lds_swizzle<D>(l32);
+    const int k_row = VT ? k_perm(l32) : l32;
+    const int k_row_off = k_row * ROWB;
+    const int k_swz = lds_swizzle<D>(k_row);
     const int grp = lane >> 4, gi = lane & 15;
     const int v_row = 4 * hw + (gi >> 2);
     const int v_swz_lo = lds_swizzle<D>(v_row), v_swz_hi = lds_swizzle<D>(v_row + 8);
     const int v_cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
     const int v_half = (gi & 1) * 8;
+    constexpr int kVtRowBytes = 64 * 2;  // a V^T row: 64 keys
+    int vt_off[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) vt_off[j] = l32 * kVtRowBytes + (((2 * j + hw) ^ vt_swizzle(l32)) << 4);
 
     auto compute = [&](const unsigned char* kb, const unsigned char* vb, int k0, int ke) {
         // ---- S^T = K Q^T: two 32-key blocks x 32 queries per wave
@@ -253,11 +293,13 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             s1 = mfma32x32x16(kb2, qf[kk], s1);
         }
 
-        // Output layout: register i of a lane holds key row 8*(i/4) + 4*hw + i%4.
+        // Output layout: register i of a lane holds S^T row 8*(i/4) + 4*hw + i%4,
+        // i.e. key 16*(i/8) + 8*hw + i%8 with the permuted K rows.
         if (k0 + BN > ke) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int kr = k0 + 8 * (i / 4) + 4 * hw + (i % 4);
+                const int kr = k0 + (VT ? 16 * (i / 8) + 8 * hw + (i % 8)
+                                        : 8 * (i / 4) + 4 * hw + (i % 4));
                 if (kr >= ke) s0[i] = kNegInf;
                 if (kr + 32 >= ke) s1[i] = kNegInf;
             }
@@ -306,6 +348,19 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
         // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*j .. 16*j + 15
         // with slot e <-> row 16*j + 4*hw + e (e < 4) or 16*j + 8 + 4*hw + e - 4
         // (e >= 4); the V^T operand reads the same keys, 4 at a time.
+        if constexpr (VT) {
+            // Row 32*d + l32 of the V^T tile, keys 16*j + 8*hw .. + 7.
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                for (int d = 0; d < DB; ++d) {
+                    const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(
+                        vb + vt_off[j] + d * 32 * kVtRowBytes);
+                    acc[d] = mfma32x32x16(vf, pf[j], acc[d]);
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -340,6 +395,7 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     while (true) {
         int r1 = r, k1 = k0, e1 = ke;
         bool more = advance(r1, k1, e1);
+        wait_lds_dma();
         __syncthreads();  // tile in buffer 0 has landed; buffer 1 is free
         if (more) issue(k1, e1, sm.k1, sm.v1);
         compute(sm.k0, sm.v0, k0, ke);
@@ -348,6 +404,7 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
 
         r1 = r; k1 = k0; e1 = ke;
         more = advance(r1, k1, e1);
+        wait_lds_dma();
         __syncthreads();  // tile in buffer 1 has landed; buffer 0 is free
         if (more) issue(k1, e1, sm.k0, sm.v0);
         compute(sm.k1, sm.v1, k0, ke);
@@ -426,12 +483,24 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(const AttnArgs a) {
                 float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
                 if (k0 + kr < ke) {
                     kv = *reinterpret_cast<const float4*>(kp + (k0 + kr) * a.k_st + c4 * 4);
-                    vv = *reinterpret_cast<const float4*>(vp + (k0 + kr) * a.v_st + c4 * 4);
+                    if (!a.v_blocked)
+                        vv = *reinterpret_cast<const float4*>(vp + (k0 + kr) * a.v_st + c4 * 4);
                 }
                 const int d0 = c4 * 4;
                 const int base = kr * RSTR + (d0 / DP) * PSTR + d0 % DP;
                 Ks[base + 0] = kv.x; Ks[base + 1] = kv.y; Ks[base + 2] = kv.z; Ks[base + 3] = kv.w;
-                Vs[base + 0] = vv.x; Vs[base + 1] = vv.y; Vs[base + 2] = vv.z; Vs[base + 3] = vv.w;
+                if (!a.v_blocked) {
+                    Vs[base + 0] = vv.x; Vs[base + 1] = vv.y; Vs[base + 2] = vv.z; Vs[base + 3] = vv.w;
+                }
+            }
+            if (a.v_blocked) {
+                // Dimension-major cache blocks: element (key, d) sits at
+                // (key / 64) * 64 * D + d * 64 + key % 64.
+                for (int e = tid; e < BN * D; e += 256) {
+                    const int d = e / BN, kr = e % BN, key = k0 + kr;
+                    Vs[kr * RSTR + (d / DP) * PSTR + d % DP] =
+                        key < ke ? vp[(key >> 6) * (64 * D) + d * 64 + (key & 63)] : 0.f;
+                }
             }
             __syncthreads();
             const int n = min(BN, ke - k0);
@@ -472,9 +541,11 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(const AttnArgs a) {
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
     const dim3 grid(a.n_qtiles * a.B * a.H), block(kBf16Threads);
     if (head_dim == 128) {
-        hipLaunchKernelGGL(attn_fwd_bf16_kernel<128>, grid, block, 0, s, a);
+        if (a.v_blocked) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false>), grid, block, 0, s, a);
     } else if (head_dim == 64) {
-        hipLaunchKernelGGL(attn_fwd_bf16_kernel<64>, grid, block, 0, s, a);
+        if (a.v_blocked) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false>), grid, block, 0, s, a);
     } else {
         return hipErrorInvalidValue;
     }

@@ -9,7 +9,8 @@
 // sits in front of a ring of W+1 chunk slots, chunk t >= 1 in slot
 // (t-1) mod (W+1); when the latest chunk is t, every cached chunk is in the
 // window of t, so the keys are the valid rows of c_0 and of each filled slot,
-// merged into contiguous ranges.
+// merged into contiguous ranges. Regions start on multiples of 8 tokens and
+// the pools hold a multiple of 64 token rows (the V pool's block size).
 
 #include <hip/hip_runtime.h>
 
@@ -54,9 +55,12 @@ struct Geo {
     int dtype;
     size_t elem;
     float scale;
-    int64_t RT, CT;  // tokens of c_0 and of a full chunk
-    int64_t capacity;
+    int64_t RT, CT;          // tokens of c_0 and of a full chunk
+    int64_t ref_cap, slot_cap;  // cache rows reserved for c_0 and for each ring slot
+    int64_t capacity;        // cache rows per (batch, head)
 };
+
+int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
 constexpr int64_t kMaxTokens = int64_t(1) << 30;
 
@@ -85,7 +89,9 @@ tm_status check_desc(const tm_attn_desc* d, Geo* g) {
     g->scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt(float(d->head_dim));
     g->RT = g->R * g->T;
     g->CT = g->C * g->T;
-    g->capacity = g->RT + (g->W + 1) * g->CT;
+    g->ref_cap = round_up(g->RT, tmk::kCacheAlign);
+    g->slot_cap = round_up(g->CT, tmk::kCacheAlign);
+    g->capacity = round_up(g->ref_cap + (g->W + 1) * g->slot_cap, tmk::kCacheBlock);
     if (g->RT > kMaxTokens || g->CT > kMaxTokens || g->capacity > kMaxTokens)
         return fail(TM_E_SHAPE, "chunk or cache too large (more than 2^30 tokens)");
     if (g->B * g->H > (int64_t(1) << 20)) return fail(TM_E_SHAPE, "batch * heads too large");
@@ -193,7 +199,7 @@ tm_status plan_stream(const Geo& g, const tm_kv_cache* c, Plan* p) {
     for (int64_t ch = std::max<int64_t>(1, t - g.W); ch <= t; ++ch) {
         const int slot = int((ch - 1) % (g.W + 1));
         if (c->slot_chunk[slot] != ch) return fail(TM_E_ORDER, "chunk %lld missing from the cache", (long long)ch);
-        const int64_t b = g.RT + slot * g.CT;
+        const int64_t b = g.ref_cap + slot * g.slot_cap;
         r.push_back({b, b + c->slot_len[slot]});
         if (ch == t) lq = c->slot_len[slot];
     }
@@ -293,6 +299,8 @@ tm_status tm_kv_cache_locate(const tm_kv_cache* cache, int32_t chunk, int32_t* t
         return fail(TM_E_ARG, "NULL argument");
     if (chunk < 0 || cache->latest < 0 || chunk > cache->latest)
         return fail(TM_E_ORDER, "chunk %d not in the cache", chunk);
+    Geo g;
+    if (check_desc(&cache->desc, &g) != TM_OK) return TM_E_ARG;
     const tm_attn_desc& d = cache->desc;
     if (chunk == 0) {
         *token_offset = 0;
@@ -301,7 +309,7 @@ tm_status tm_kv_cache_locate(const tm_kv_cache* cache, int32_t chunk, int32_t* t
     }
     const int slot = (chunk - 1) % (d.window + 1);
     if (cache->slot_chunk[slot] != chunk) return fail(TM_E_ORDER, "chunk %d was evicted", chunk);
-    *token_offset = d.ref_frames * d.tokens_per_frame + slot * d.chunk_frames * d.tokens_per_frame;
+    *token_offset = int32_t(g.ref_cap + slot * g.slot_cap);
     *n_tok = cache->slot_len[slot];
     return TM_OK;
 }
@@ -329,9 +337,10 @@ tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const v
     if ((st = check_ptr(cache->k_pool, pool_bytes, "k_pool")) != TM_OK) return st;
     if ((st = check_ptr(cache->v_pool, pool_bytes, "v_pool")) != TM_OK) return st;
     const int slot = chunk == 0 ? -1 : int((chunk - 1) % (g.W + 1));
-    const int64_t offset = chunk == 0 ? 0 : g.RT + slot * g.CT;
+    const int64_t offset = chunk == 0 ? 0 : g.ref_cap + slot * g.slot_cap;
     const hipError_t e = tmk::launch_kv_append(k, v, cache->k_pool, cache->v_pool, int(g.B), n_tok,
-                                              int(g.H), int(g.D * g.elem), g.capacity, offset, stream);
+                                              int(g.H), int(g.D), int(g.elem), g.capacity, offset,
+                                              stream);
     if (e != hipSuccess) return fail(TM_E_DEVICE, "kv_append launch: %s", hipGetErrorString(e));
     if (chunk == 0) {
         tm_kv_cache_reset(cache);
@@ -369,7 +378,9 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
         a.v = cache->v_pool;
         a.k_sb = a.v_sb = g.H * g.capacity * g.D;
         a.k_sh = a.v_sh = g.capacity * g.D;
-        a.k_st = a.v_st = g.D;
+        a.k_st = g.D;
+        a.v_st = 0;
+        a.v_blocked = 1;
         kv_bytes = tm_kv_cache_bytes(desc);
     } else {
         a.k = k;

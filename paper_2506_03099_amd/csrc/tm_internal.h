@@ -14,7 +14,18 @@ constexpr int kMaxRanges = 16;  // key ranges of one query segment (>= TM_MAX_WI
 constexpr int kTileRowsBf16 = 256;
 constexpr int kTileRowsF32 = 64;
 
+// KV-cache pools are organised in blocks of this many token rows. The V pool
+// stores each block dimension-major: [D][kCacheBlock] per (batch, head, block),
+// so that the attention kernel's V^T operand is a contiguous 16-byte read.
+constexpr int kCacheBlock = 64;
+// Cache regions (c_0 and every ring slot) start on multiples of this many
+// tokens, so that every 16-byte group of a V block row belongs to one region.
+constexpr int kCacheAlign = 8;
+
 // One attention launch. Element strides (not bytes) for batch, token and head.
+// With v_blocked != 0, v is a cache V pool: element (token t, dim d) of a head
+// sits at (t / 64) * 64 * D + d * 64 + t % 64 from the head's base, v_st is
+// unused, and every key range starts on a multiple of kCacheAlign.
 struct AttnArgs {
     const void* q;
     const void* k;
@@ -25,6 +36,7 @@ struct AttnArgs {
     int64_t k_sb, k_st, k_sh;
     int64_t v_sb, v_st, v_sh;
     int64_t o_sb, o_st, o_sh;
+    int32_t v_blocked;
     int32_t B, H, Lq;
     float scale_log2;  // softmax scale * log2(e)
     int32_t n_qtiles;  // query tiles per (batch, head)
@@ -47,11 +59,13 @@ struct AttnArgs {
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 
-// Copy n_tok tokens of K and V from [B, n_tok, H, D] into pools laid out
-// [B, H, capacity, D] at token row `tok_offset`. `row_bytes` = D * element
-// size (a multiple of 16).
+// Copy n_tok tokens of K and V from [B, n_tok, H, D] into the cache pools at
+// token row `tok_offset` (a multiple of kCacheAlign): K into [B, H, capacity,
+// D], V into [B, H, capacity / 64, D, 64]. The V columns from n_tok up to the
+// next multiple of kCacheAlign are written as zeros. `capacity` is a multiple
+// of kCacheBlock; elem_bytes is 2 or 4.
 hipError_t launch_kv_append(const void* k_src, const void* v_src, void* k_pool, void* v_pool,
-                            int B, int n_tok, int H, int row_bytes, int64_t capacity,
+                            int B, int n_tok, int H, int D, int elem_bytes, int64_t capacity,
                             int64_t tok_offset, hipStream_t s);
 
 }  // namespace tmk

@@ -146,16 +146,19 @@ def tm_allowed_pairs(desc: tm_attn_desc, q_chunk: int, cache=None, n_frames: int
 
 class KVCache:
     """A ``tm_kv_cache`` handle together with the torch tensors that own its
-    K and V pools (``[B, H, capacity, D]`` each)."""
+    pools: K ``[B, H, capacity, D]``, V ``[B, H, capacity // 64, D, 64]``
+    (64-token blocks stored dimension-major)."""
 
     def __init__(self, desc: tm_attn_desc, device="cuda", k_pool=None, v_pool=None):
         self.desc = desc
         cap = tm_kv_cache_tokens(desc)
         if cap <= 0:
             raise TMError(TM_E_SHAPE, "invalid descriptor")
-        shape = (desc.batch, desc.heads, cap, desc.head_dim)
-        self.k_pool = k_pool if k_pool is not None else torch.empty(shape, dtype=desc.torch_dtype, device=device)
-        self.v_pool = v_pool if v_pool is not None else torch.empty(shape, dtype=desc.torch_dtype, device=device)
+        B, H, D, dt = desc.batch, desc.heads, desc.head_dim, desc.torch_dtype
+        self.k_pool = k_pool if k_pool is not None else torch.empty(
+            (B, H, cap, D), dtype=dt, device=device)
+        self.v_pool = v_pool if v_pool is not None else torch.empty(
+            (B, H, cap // 64, D, 64), dtype=dt, device=device)
         h = ctypes.c_void_p()
         _check(lib().tm_kv_cache_create(ctypes.byref(desc), _ptr(self.k_pool), _ptr(self.v_pool),
                                         ctypes.byref(h)))

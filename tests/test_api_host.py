@@ -47,12 +47,18 @@ def _desc(tm, **kw):
 
 
 def test_cache_size_arithmetic(tm):
+    # c_0 and each ring slot take their token count rounded up to 8; the total
+    # is rounded up to the 64-token block of the V pool.
     d = _desc(tm)
-    assert tm.tm_kv_cache_tokens(d) == 1560 + 2 * 4680 == 10920
-    assert tm.tm_kv_cache_bytes(d) == 40 * 10920 * 128 * 2
+    assert tm.tm_kv_cache_tokens(d) == 10944  # 1560 + 2 * 4680 = 10920 -> 171 blocks of 64
+    assert tm.tm_kv_cache_bytes(d) == 40 * 10944 * 128 * 2
     d2 = _desc(tm, batch=2, tokens_per_frame=3600, dtype=tm.TM_F32, window=3)
-    assert tm.tm_kv_cache_tokens(d2) == 3600 + 4 * 10800
-    assert tm.tm_kv_cache_bytes(d2) == 2 * 40 * (3600 + 4 * 10800) * 128 * 4
+    assert tm.tm_kv_cache_tokens(d2) == 46848  # 3600 + 4 * 10800 = 46800 -> 732 blocks
+    assert tm.tm_kv_cache_bytes(d2) == 2 * 40 * 46848 * 128 * 4
+    d3 = _desc(tm, tokens_per_frame=5, chunk_frames=3, ref_frames=1, window=2)
+    assert tm.tm_kv_cache_tokens(d3) == 64  # 8 + 3 * 16 = 56 -> one block
+    d4 = _desc(tm, tokens_per_frame=7, chunk_frames=10, ref_frames=3, window=12)
+    assert tm.tm_kv_cache_tokens(d4) == 960  # 24 + 13 * 72 = 960
 
 
 @pytest.mark.parametrize("kw", [dict(head_dim=96), dict(head_dim=0), dict(batch=0),

@@ -61,6 +61,11 @@ def test_kv_append_ring_is_bitwise_and_evicts(tm, dtype, W):
     exp_v = cache.v_pool.view(ib).cpu().numpy().copy()
     rng = np.random.default_rng(W)
     RT, CT = R * T, C * T
+    # Documented layout: c_0 at row 0, ring slot s at row 16 + 16 * s (c_0 and
+    # chunks of 10 tokens each take 16 rows); V element (row t, dim d) at
+    # block t // 64, row d, column t % 64; the V columns from the chunk's end
+    # to the next multiple of 8 are zeros.
+    assert cache.capacity == 64 and exp_v.shape == (B, H, 1, D, 64)
     seq = [(0, RT), (1, CT), (1, CT), (2, CT), (3, 3), (4, CT), (5, 7), (6, 1)]
     history = {}
     for chunk, n in seq:
@@ -68,11 +73,13 @@ def test_kv_append_ring_is_bitwise_and_evicts(tm, dtype, W):
             torch.bfloat16 if dtype == "bf16" else torch.float32).cuda()
         v = torch.from_numpy(rng.standard_normal((B, n, H, D)).astype(np.float32)).to(k.dtype).cuda()
         tm.tm_kv_append(cache, chunk, k, v)
-        off = 0 if chunk == 0 else RT + ((chunk - 1) % (W + 1)) * CT
+        off = 0 if chunk == 0 else 16 + ((chunk - 1) % (W + 1)) * 16
         kh = k.view(ib).cpu().numpy()
         vh = v.view(ib).cpu().numpy()
         exp_k[:, :, off:off + n, :] = kh.transpose(0, 2, 1, 3)
-        exp_v[:, :, off:off + n, :] = vh.transpose(0, 2, 1, 3)
+        n8 = (n + 7) // 8 * 8
+        exp_v[:, :, 0, :, off:off + n8] = 0
+        exp_v[:, :, 0, :, off:off + n] = vh.transpose(0, 2, 3, 1)
         torch.cuda.synchronize()
         assert np.array_equal(cache.k_pool.view(ib).cpu().numpy(), exp_k)
         assert np.array_equal(cache.v_pool.view(ib).cpu().numpy(), exp_v)
@@ -272,6 +279,35 @@ def test_repeatable_bitwise_and_output_canaries(tm):
         torch.cuda.synchronize()
         assert torch.equal(o, first)
     assert torch.all(buf[:2048] == 7.0) and torch.all(buf[2048 + n:] == 7.0)
+
+
+@pytest.mark.parametrize("form", ["cache", "sequence"])
+def test_first_call_equals_repeated_calls_480p(tm, form):
+    """The first launch on freshly written K/V (cold caches, slow tile loads)
+    must give bit for bit what repeated launches give: a tile read from LDS
+    before its loads have landed would show up here."""
+    w = WORKLOADS["wan14b_480p_stream"]
+    desc = _desc(tm, w)
+    say(f"first call vs repeated, 480p chunk 1, {form}")
+    cache = tm.KVCache(desc) if form == "cache" else None
+    ks, vs = [], []
+    for t in range(2):
+        q, k, v = chunk_to_dev(draw_chunk(w, t, step=1), "bf16")
+        ks.append(k); vs.append(v)
+        if cache is not None:
+            tm.tm_kv_append(cache, t, k, v)
+    if cache is not None:
+        run = lambda: tm.tm_sparse_causal_attn_fwd(desc, q, 1, cache=cache)
+    else:
+        K, V = (torch.cat(x, dim=1).contiguous() for x in (ks, vs))
+        frames = w.ref_frames + w.chunk_frames
+        run = lambda: tm.tm_sparse_causal_attn_fwd(desc, q, 1, k=K, v=V, n_frames=frames)
+    first = run()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        again = run()
+        torch.cuda.synchronize()
+        assert torch.equal(first, again)
 
 
 def test_streaming_equals_full_sequence_on_gpu(tm):
