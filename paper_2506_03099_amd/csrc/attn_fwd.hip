@@ -52,11 +52,52 @@ constexpr int kBf16Threads = 512;
 // s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
 constexpr int kWaitVmcnt0 = 0x0F70;
 
+// 32-bit LDS byte address of a pointer into __shared__ memory, made
+// wave-uniform (it is loaded into M0).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+        (const __attribute__((address_space(3))) unsigned char*)(p)));
+    return __builtin_amdgcn_readfirstlane(a);
+}
+
+// A pointer that is the same in every lane, held in scalar registers.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Direct global->LDS load (global_load_lds_dwordx4) of 16 bytes per lane
+// from the wave-uniform base `sbase` plus the lane's byte offset `voff`; lane
+// l's bytes land at LDS address lds_base + 16 * l (M0 = lds_base, restored
+// afterwards). Written as inline assembly so that these loads stay out of the
+// compiler's wait bookkeeping, which would otherwise make LDS reads of one
+// tile wait for the loads of later tiles; the kernel waits for them
+// explicitly (below) before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(voff), "s"(sbase));
+}
+
 // Wait until every direct global->LDS load issued by this wave has written
 // LDS. The barrier that publishes a tile only orders LDS operations; the
 // direct loads count as vector-memory operations, so each wave waits for its
 // own before the barrier, and after the barrier the whole tile is in place.
 __device__ __forceinline__ void wait_lds_dma() { __builtin_amdgcn_s_waitcnt(kWaitVmcnt0); }
+// The same, except that the newest N direct loads may still be in flight
+// (vector-memory operations complete in issue order for this count).
+template <int N>
+__device__ __forceinline__ void wait_lds_dma_but() {
+    static_assert(N >= 0 && N < 16, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0 | N);
+}
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
 // Renumber them so that consecutive logical ids (the query tiles of one head,
@@ -172,14 +213,7 @@ __device__ __forceinline__ int vt_swizzle(int d) { return (d >> 1) & 7; }
 // feeds to a 16-key MFMA step are 8 consecutive keys.
 __device__ __forceinline__ int k_perm(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
-template <int D>
-struct Bf16Smem {
-    static constexpr int kTileBytes = 64 * D * 2;
-    __attribute__((aligned(1024))) unsigned char k0[kTileBytes];
-    __attribute__((aligned(1024))) unsigned char k1[kTileBytes];
-    __attribute__((aligned(1024))) unsigned char v0[kTileBytes];
-    __attribute__((aligned(1024))) unsigned char v1[kTileBytes];
-};
+
 
 template <int D, bool VT>
 __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const AttnArgs a) {
@@ -195,7 +229,12 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     static_assert(NI * kBf16Threads * 16 == TILEB, "tile must split evenly over the threads");
     static_assert(BM == NW * 32, "one 32-row query block per wave");
 
-    __shared__ Bf16Smem<D> sm;
+    // Three K and three V tiles, each its own LDS object so that the compiler
+    // can tell a tile being read from the tiles whose loads are in flight.
+    __shared__ __attribute__((aligned(1024))) unsigned char k_t0[TILEB], k_t1[TILEB], k_t2[TILEB];
+    __shared__ __attribute__((aligned(1024))) unsigned char v_t0[TILEB], v_t1[TILEB], v_t2[TILEB];
+    unsigned char* const kbuf[3] = {k_t0, k_t1, k_t2};
+    unsigned char* const vbuf[3] = {v_t0, v_t1, v_t2};
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -220,29 +259,47 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     // A V^T tile takes, for each dimension d, the 8-key groups of the tile from
     // the cache's V block(s); groups past the range end re-read the group that
     // holds the range's last key (its other columns are the append's zeros).
-    auto issue = [&](int k0, int ke, unsigned char* kd, unsigned char* vd) {
+    // This wave's share of one tile's direct loads: 2 * NI loads of one 1 KB
+    // LDS block each, the first NI for the K tile, the rest for the V tile.
+    // Lane offsets from the tile's scalar bases are kept in ld_off; they only
+    // change with k0 mod 64 (V^T) or for a range's last tile (rows past the
+    // range end re-read its last row, V^T groups past it the group holding
+    // its last key), so plan_loads recomputes them only then.
+    uint32_t ld_off[2 * NI];
+    int ld_o = -1;  // k0 mod 64 that ld_off was planned for; -1 after a last tile
+    auto plan_loads = [&](int k0, int ke) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int blk = i * NW + wave;  // 1 KB block of the tile
-            const int ch = blk * 64 + lane;
-            const int row = ch / CPR;
-            const int gc = (ch % CPR) ^ lds_swizzle<D>(row);
-            const int key = min(k0 + row, ke - 1);
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(kp + key * a.k_st + gc * 8),
-                (__attribute__((address_space(3))) void*)(kd + blk * 1024), 16, 0, 0);
-            const __bf16* vsrc;
-            if constexpr (VT) {
-                const int d = ch >> 3;
-                const int g = min(k0 + 8 * ((ch & 7) ^ vt_swizzle(d)), (ke - 1) & ~7);
-                vsrc = vp + (g >> 6) * (64 * D) + d * 64 + (g & 63);
+        for (int i = 0; i < 2 * NI; ++i) {
+            const int ch = ((i % NI) * NW + wave) * 64 + lane;
+            if (i < NI || !VT) {
+                const int row = min(ch / CPR, ke - 1 - k0);
+                const int gc = (ch % CPR) ^ lds_swizzle<D>(ch / CPR);
+                const int64_t st = i < NI ? a.k_st : a.v_st;
+                ld_off[i] = static_cast<uint32_t>((row * st + gc * 8) * 2);
             } else {
-                vsrc = vp + key * a.v_st + gc * 8;
+                const int d = ch >> 3;
+                const int b0 = k0 & ~63;  // first cache block of the tile
+                const int g = min(k0 + 8 * ((ch & 7) ^ vt_swizzle(d)), (ke - 1) & ~7) - b0;
+                ld_off[i] = static_cast<uint32_t>(((g >> 6) * (64 * D) + d * 64 + (g & 63)) * 2);
             }
-            __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)vsrc,
-                                             (__attribute__((address_space(3))) void*)(vd + blk * 1024),
-                                             16, 0, 0);
         }
+        ld_o = k0 + BN <= ke ? (k0 & 63) : -1;
+    };
+    auto prepare_loads = [&](int k0, int ke) __attribute__((always_inline)) {
+        if (k0 + BN > ke || (k0 & 63) != ld_o) plan_loads(k0, ke);
+    };
+    auto issue_one = [&](int i, int k0, unsigned char* kd, unsigned char* vd)
+        __attribute__((always_inline)) {
+        const int blk = (i % NI) * NW + wave;
+        const void* base = i < NI ? static_cast<const void*>(kp + static_cast<int64_t>(k0) * a.k_st)
+                           : VT   ? static_cast<const void*>(vp + static_cast<int64_t>(k0 & ~63) * D)
+                                  : static_cast<const void*>(vp + static_cast<int64_t>(k0) * a.v_st);
+        lds_dma16(uniform_ptr(base), ld_off[i], lds_addr((i < NI ? kd : vd) + blk * 1024));
+    };
+    auto issue = [&](int k0, int ke, unsigned char* kd, unsigned char* vd) __attribute__((always_inline)) {
+        prepare_loads(k0, ke);
+#pragma unroll
+        for (int i = 0; i < 2 * NI; ++i) issue_one(i, k0, kd, vd);
     };
 
     // Q^T operand (B of the S^T MFMA): lane holds q[row][16*kk + 8*hw .. +8].
@@ -257,6 +314,9 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             qf[kk] = bf16x8_t{};
         }
     }
+    // The Q loads land before any direct load is issued, so no wait that the
+    // compiler places for them can be miscounted.
+    wait_lds_dma();
 
     f32x16_t acc[DB];
 #pragma unroll
@@ -281,17 +341,38 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
 #pragma unroll
     for (int j = 0; j < 4; ++j) vt_off[j] = l32 * kVtRowBytes + (((2 * j + hw) ^ vt_swizzle(l32)) << 4);
 
-    auto compute = [&](const unsigned char* kb, const unsigned char* vb, int k0, int ke) {
+    // One tile: keys [k0, ke) from buffers kb, vb. The loads of the next tile
+    // (keys from nk0 into nkd, nvd) are spread over the score MFMAs, so that
+    // no wave stalls on a full load queue while the others also issue theirs.
+    constexpr int kAhead = 4;  // LDS operand reads run this many MFMAs ahead
+    auto compute = [&](const unsigned char* kb, const unsigned char* vb, int k0, int ke, int nk0,
+                       int nke, unsigned char* nkd, unsigned char* nvd) __attribute__((always_inline)) {
         // ---- S^T = K Q^T: two 32-key blocks x 32 queries per wave
         f32x16_t s0 = f32x16_t{}, s1 = f32x16_t{};
+        constexpr int kLoadEvery = KK / (2 * NI);
+        static_assert(kLoadEvery >= 1 && kLoadEvery * 2 * NI == KK, "loads must spread evenly");
+        bf16x8_t kf[2 * KK];
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const int off = k_row_off + (((2 * kk + hw) ^ k_swz) << 4);
-            const bf16x8_t ka = *reinterpret_cast<const bf16x8_t*>(kb + off);
-            const bf16x8_t kb2 = *reinterpret_cast<const bf16x8_t*>(kb + off + 32 * ROWB);
-            s0 = mfma32x32x16(ka, qf[kk], s0);
-            s1 = mfma32x32x16(kb2, qf[kk], s1);
+            kf[2 * kk] = *reinterpret_cast<const bf16x8_t*>(kb + off);
+            kf[2 * kk + 1] = *reinterpret_cast<const bf16x8_t*>(kb + off + 32 * ROWB);
         }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            s0 = mfma32x32x16(kf[2 * kk], qf[kk], s0);
+            s1 = mfma32x32x16(kf[2 * kk + 1], qf[kk], s1);
+            if (kk % kLoadEvery == 0) issue_one(kk / kLoadEvery, nk0, nkd, nvd);
+        }
+        // Each K fragment is read kAhead MFMAs before the MFMA that uses it,
+        // so the LDS latency hides behind the wave's own MFMAs.
+        __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);  // LDS reads
+#pragma unroll
+        for (int i = 0; i < 2 * KK - kAhead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
 
         // Output layout: register i of a lane holds S^T row 8*(i/4) + 4*hw + i%4,
         // i.e. key 16*(i/8) + 8*hw + i%8 with the permuted K rows.
@@ -305,18 +386,42 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             }
         }
 
-        // ---- online softmax. The running max m_run is shared by the two
-        // half-waves holding a query's scores. It is only raised (and the
-        // accumulator rescaled) when some score exceeds it by more than 2^8,
-        // which each lane can tell from its own 32 scores; only then are the
-        // two halves' maxima combined, so the common path has no cross-lane
-        // step and m_run stays identical in both halves.
-        float mx = s0[0];
+        // ---- online softmax against the running max m_run, which is shared
+        // by the two half-waves holding a query's scores. The common path takes
+        // no maximum: P = exp2(S * c - m_run) is formed against the current
+        // m_run and kept unless some lane's sum of its 32 values exceeds 2^16
+        // (or is not finite), i.e. unless a score exceeds m_run by more than 16
+        // in the log2 domain. Otherwise (always on the first tile, rarely
+        // after) the exact maximum of both halves is taken, O and the row sum
+        // are rescaled and P is formed again. P is at most 2^16 either way, so
+        // it and O keep their full relative precision far from overflow.
+        bf16x8_t pf[4];
+        const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+        auto form_p = [&](float neg_m) __attribute__((always_inline)) -> float {
 #pragma unroll
-        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
+            for (int i = 0; i < 16; ++i) {
+                pf[i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s0[i], c, neg_m)));
+                pf[2 + i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s1[i], c, neg_m)));
+            }
+            // Row sum of the bf16-rounded P that is multiplied into V.
+            float l = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-        if (__any(mx * c > m_run + 8.f)) {
+            for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const bf16x2_t pp = {pf[j][2 * e], pf[j][2 * e + 1]};
+                    l = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l, false);
+                }
+            }
+            return l;
+        };
+        float lt = form_p(-m_run);
+        if (__any(!(lt <= 0x1p16f))) {
+            float mx = s0[0];
+#pragma unroll
+            for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
             const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx),
                                                              __float_as_uint(mx), false, false);
             mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // both halves
@@ -326,39 +431,33 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             l_run *= alpha;
 #pragma unroll
             for (int d = 0; d < DB; ++d) acc[d] *= alpha;
+            lt = form_p(-m_run);
         }
-        const float neg_m = -m_run;
-        bf16x8_t pf[4];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            pf[i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s0[i], c, neg_m)));
-            pf[2 + i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s1[i], c, neg_m)));
-        }
-        // Row sum of the bf16-rounded P that is multiplied into V, two at a time.
-        const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const bf16x2_t pp = {pf[j][2 * e], pf[j][2 * e + 1]};
-                l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l_run, false);
-            }
-        }
+        l_run += lt;
 
         // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*j .. 16*j + 15
         // with slot e <-> row 16*j + 4*hw + e (e < 4) or 16*j + 8 + 4*hw + e - 4
         // (e >= 4); the V^T operand reads the same keys, 4 at a time.
         if constexpr (VT) {
-            // Row 32*d + l32 of the V^T tile, keys 16*j + 8*hw .. + 7.
+            // Row 32*d + l32 of the V^T tile, keys 16*j + 8*hw .. + 7, each
+            // fragment read kAhead MFMAs before its MFMA.
+            bf16x8_t vf[4 * DB];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                for (int d = 0; d < DB; ++d) {
-                    const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(
-                        vb + vt_off[j] + d * 32 * kVtRowBytes);
-                    acc[d] = mfma32x32x16(vf, pf[j], acc[d]);
-                }
+                for (int d = 0; d < DB; ++d)
+                    vf[j * DB + d] = *reinterpret_cast<const bf16x8_t*>(vb + vt_off[j] + d * 32 * kVtRowBytes);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int d = 0; d < DB; ++d) acc[d] = mfma32x32x16(vf[j * DB + d], pf[j], acc[d]);
+            __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+            for (int i = 0; i < 4 * DB - kAhead; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
+            __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
             return;
         }
 #pragma unroll
@@ -376,41 +475,53 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
         }
     };
 
-    // Double-buffered main loop, unrolled by two so each buffer is named
-    // statically: the loads of tile t+1 are in flight while tile t computes.
-    int r = 0;
-    int k0 = range_begin(a, tr, 0);
-    int ke = range_end(a, tr, 0);
-    issue(k0, ke, sm.k0, sm.v0);
-    auto advance = [&](int& rr, int& kk0, int& kke) -> bool {
-        kk0 += BN;
-        if (kk0 >= kke) {
-            ++rr;
-            if (rr >= tr.n) return false;
-            kk0 = range_begin(a, tr, rr);
-            kke = range_end(a, tr, rr);
-        }
-        return true;
+    // Triple-buffered main loop, unrolled by three so each buffer is named
+    // statically: tile t sits in buffer t % 3 and is computed while tiles t+1
+    // and t+2 load (the loads of tile t+2 are issued during tile t, into the
+    // buffer of tile t-1, which every wave finished before the barrier at the
+    // top of iteration t). Past the last tile the loads re-read the last tile
+    // (harmless; no one reads those buffers again), which keeps the code free
+    // of branches. Each wave issues 2 * NI loads per tile, so waiting until
+    // at most 2 * NI are outstanding leaves only tile t+1's in flight.
+    struct KeyTile {
+        int r, k0, ke;
     };
-    while (true) {
-        int r1 = r, k1 = k0, e1 = ke;
-        bool more = advance(r1, k1, e1);
-        wait_lds_dma();
-        __syncthreads();  // tile in buffer 0 has landed; buffer 1 is free
-        if (more) issue(k1, e1, sm.k1, sm.v1);
-        compute(sm.k0, sm.v0, k0, ke);
-        if (!more) break;
-        r = r1; k0 = k1; ke = e1;
-
-        r1 = r; k1 = k0; e1 = ke;
-        more = advance(r1, k1, e1);
-        wait_lds_dma();
-        __syncthreads();  // tile in buffer 1 has landed; buffer 0 is free
-        if (more) issue(k1, e1, sm.k0, sm.v0);
-        compute(sm.k1, sm.v1, k0, ke);
-        if (!more) break;
-        r = r1; k0 = k1; ke = e1;
+    auto advance = [&](KeyTile t) __attribute__((always_inline)) {
+        KeyTile u = t;
+        u.k0 += BN;
+        if (u.k0 >= u.ke) {
+            if (u.r + 1 >= tr.n) return t;  // past the end: stay on the last tile
+            u.r += 1;
+            u.k0 = range_begin(a, tr, u.r);
+            u.ke = range_end(a, tr, u.r);
+        }
+        return u;
+    };
+    int n = 0;
+    for (int r = 0; r < tr.n; ++r) n += (range_end(a, tr, r) - range_begin(a, tr, r) + BN - 1) / BN;
+    KeyTile cur{0, range_begin(a, tr, 0), range_end(a, tr, 0)};
+    KeyTile ld1 = advance(cur);  // tile t+1
+    issue(cur.k0, cur.ke, kbuf[0], vbuf[0]);
+    issue(ld1.k0, ld1.ke, kbuf[1], vbuf[1]);
+    KeyTile ld2 = advance(ld1);  // tile t+2
+    auto step = [&](int b) __attribute__((always_inline)) {
+        prepare_loads(ld2.k0, ld2.ke);
+        wait_lds_dma_but<2 * NI>();
+        __syncthreads();  // tile t is in buffer b for every wave
+        const int bn = b == 0 ? 2 : b - 1;  // (t + 2) % 3
+        compute(kbuf[b], vbuf[b], cur.k0, cur.ke, ld2.k0, ld2.ke, kbuf[bn], vbuf[bn]);
+        cur = ld1;
+        ld1 = ld2;
+        ld2 = advance(ld2);
+    };
+    for (int t = 0; t < n; t += 3) {
+        step(0);
+        if (t + 1 >= n) break;
+        step(1);
+        if (t + 2 >= n) break;
+        step(2);
     }
+    wait_lds_dma();  // no load may still be writing LDS when the workgroup ends
 
     // ---- epilogue: normalise, round to bf16, store rows inside the tile
     const float l_tot = l_run + __shfl_xor(l_run, 32);
