@@ -62,6 +62,8 @@ def parse():
                    help="chunks of the streaming loop measured for ms per chunk (0 = skip)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="time budget of the CPU oracle sample (0 = skip)")
+    p.add_argument("--other-workloads", type=int, default=1,
+                   help="also time the 480p full sequence and the 720p two-stream chunk (0 = skip)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run one plain 512 MiB device copy (for counter calibration)")
     return p.parse_args()
@@ -189,8 +191,27 @@ def main():
             "traffic": measured_traffic(),
         },
     }
+    # cold: the attention launch after 1 GiB has been written, which evicts the
+    # chunk's K/V from the Infinity Cache and the L2s
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    cold = []
+    for _ in range(5):
+        flush.fill_(1)
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a_.record(stream)
+        tm.tm_sparse_causal_attn_fwd(desc, q, cur, cache=cache, o=o)
+        b_.record(stream)
+        torch.cuda.synchronize()
+        cold.append(a_.elapsed_time(b_))
+    del flush
+    result["attn_cold_ms"] = round(float(np.median(cold)), 4)
+    result["attn_cold_tflops"] = round(flops / (np.median(cold) * 1e-3) / 1e12, 2)
     del cache, dev, chunks
     torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- other workloads
+    if args.other_workloads:
+        result["other_workloads"] = other_workloads(torch, tm, WORKLOADS, stream)
 
     # ---------------------------------------------------------------- streaming loop
     if args.stream_chunks > 0:
@@ -202,6 +223,76 @@ def main():
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def timing_inputs(torch, shape, seed):
+    """Seeded synthetic q, k, v of the given [B, L, H, D] shape drawn on the
+    GPU (the same distribution as the parity inputs: N(0,1), q and k
+    RMS-normalised per token and head, rounded to bf16); for timing only."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    out = []
+    for i in range(3):
+        x = torch.randn(shape, generator=g, device="cuda", dtype=torch.float32)
+        if i < 2:
+            x = x / x.pow(2).mean(-1, keepdim=True).sqrt()
+        out.append(x.to(torch.bfloat16))
+        del x
+    return out
+
+
+def other_workloads(torch, tm, workloads, stream, reps=10):
+    """Attention TFLOP/s (unmasked pairs) of the 480p full sequence (21 latent
+    frames, one call over all 32760 queries) and of the 720p chunk with two
+    streams (append + attention over a cache of c_0 and the previous chunk)."""
+    def time_call(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    out = {}
+    w = workloads["wan14b_480p_full_sequence"]
+    desc = workload_desc(tm, w)
+    L = w.n_frames * w.tokens_per_frame
+    q, k, v = timing_inputs(torch, (w.batch, L, w.heads, w.head_dim), 3)
+    o = torch.empty_like(q)
+    pairs = tm.tm_allowed_pairs(desc, -1, None, w.n_frames)
+    flops = 4.0 * w.head_dim * w.heads * w.batch * pairs
+    ms = time_call(lambda: tm.tm_sparse_causal_attn_fwd(desc, q, -1, k=k, v=v,
+                                                        n_frames=w.n_frames, o=o))
+    out[w.name] = {"queries": L, "keys": L, "allowed_pairs_per_head": int(pairs),
+                   "density": round(pairs / float(L * L), 4), "ms": round(ms, 4),
+                   "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+                   "dense_equivalent_tflops": round(4.0 * w.head_dim * w.heads * L * L /
+                                                    (ms * 1e-3) / 1e12, 2)}
+    del q, k, v, o
+    torch.cuda.empty_cache()
+
+    w = workloads["wan14b_720p_chunk_b2"]
+    desc = workload_desc(tm, w)
+    cache = tm.KVCache(desc)
+    shape = lambda n: (w.batch, n, w.heads, w.head_dim)
+    ref = timing_inputs(torch, shape(w.ref_frames * w.tokens_per_frame), 50)
+    prev = timing_inputs(torch, shape(w.chunk_frames * w.tokens_per_frame), 51)
+    q, k, v = timing_inputs(torch, shape(w.chunk_frames * w.tokens_per_frame), 52)
+    tm.tm_kv_append(cache, 0, ref[1], ref[2])
+    tm.tm_kv_append(cache, 1, prev[1], prev[2])
+    tm.tm_kv_append(cache, 2, k, v)
+    o = torch.empty_like(q)
+    pairs = tm.tm_allowed_pairs(desc, 2, cache)
+    flops = 4.0 * w.head_dim * w.heads * w.batch * pairs
+    ms = time_call(lambda: tm.tm_sparse_causal_attn_fwd(desc, q, 2, cache=cache, o=o))
+    out[w.name] = {"batch": w.batch, "queries": int(q.shape[1]), "keys": int(pairs // q.shape[1]),
+                   "ms": round(ms, 4), "tflops": round(flops / (ms * 1e-3) / 1e12, 2)}
+    del cache, ref, prev, q, k, v, o
+    torch.cuda.empty_cache()
+    return out
 
 
 def stream_loop(torch, tm, w, n_chunks, stream):

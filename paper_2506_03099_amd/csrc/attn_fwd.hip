@@ -52,8 +52,7 @@ constexpr int kBf16Threads = 512;
 // s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
 constexpr int kWaitVmcnt0 = 0x0F70;
 
-// 32-bit LDS byte address of a pointer into __shared__ memory, made
-// wave-uniform (it is loaded into M0).
+// 32-bit LDS byte address of a __shared__ object, made wave-uniform.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
         (const __attribute__((address_space(3))) unsigned char*)(p)));
@@ -68,22 +67,30 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
     return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-// Direct global->LDS load (global_load_lds_dwordx4) of 16 bytes per lane
-// from the wave-uniform base `sbase` plus the lane's byte offset `voff`; lane
-// l's bytes land at LDS address lds_base + 16 * l (M0 = lds_base, restored
-// afterwards). Written as inline assembly so that these loads stay out of the
-// compiler's wait bookkeeping, which would otherwise make LDS reads of one
-// tile wait for the loads of later tiles; the kernel waits for them
-// explicitly (below) before the barrier that publishes a tile.
-__device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds_base) {
+// Two direct global->LDS loads (global_load_lds_dwordx4) of 16 bytes per lane:
+// load n reads from the wave-uniform base sbase<n> plus the lane's byte offset
+// voff<n>, and lane l's bytes land at LDS address lds<n> + 16 * l. The LDS
+// address goes through M0 (saved and restored); an SALU write of M0 needs one
+// wait state before an LDS-DMA instruction (or anything else) reads it, hence
+// the s_nop after each write. Written as inline assembly so that these loads
+// stay out of the compiler's wait bookkeeping, which would otherwise make LDS
+// reads of one tile wait for the loads of later tiles; the kernel waits for
+// them explicitly before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_dma16x2(const void* sbase0, uint32_t voff0, uint32_t lds0,
+                                            const void* sbase1, uint32_t voff1, uint32_t lds1) {
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
         "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
         "global_load_lds_dwordx4 %2, %3\n\t"
-        "s_mov_b32 m0, %0"
+        "s_mov_b32 m0, %4\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %5, %6\n\t"
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0"
         : "=&s"(saved)
-        : "s"(lds_base), "v"(voff), "s"(sbase));
+        : "s"(lds0), "v"(voff0), "s"(sbase0), "s"(lds1), "v"(voff1), "s"(sbase1));
 }
 
 // Wait until every direct global->LDS load issued by this wave has written
@@ -91,6 +98,14 @@ __device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint
 // direct loads count as vector-memory operations, so each wave waits for its
 // own before the barrier, and after the barrier the whole tile is in place.
 __device__ __forceinline__ void wait_lds_dma() { __builtin_amdgcn_s_waitcnt(kWaitVmcnt0); }
+// Wait until at most N LDS operations (and scalar loads) of this wave are
+// outstanding; vector-memory and export counts are left unconstrained.
+template <int N>
+__device__ __forceinline__ void wait_lds_reads() {
+    static_assert(N >= 0 && N < 16, "lgkmcnt field");
+    __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
+}
+
 // The same, except that the newest N direct loads may still be in flight
 // (vector-memory operations complete in issue order for this count).
 template <int N>
@@ -235,6 +250,8 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     __shared__ __attribute__((aligned(1024))) unsigned char v_t0[TILEB], v_t1[TILEB], v_t2[TILEB];
     unsigned char* const kbuf[3] = {k_t0, k_t1, k_t2};
     unsigned char* const vbuf[3] = {v_t0, v_t1, v_t2};
+    const uint32_t lds_k[3] = {lds_addr(k_t0), lds_addr(k_t1), lds_addr(k_t2)};
+    const uint32_t lds_v[3] = {lds_addr(v_t0), lds_addr(v_t1), lds_addr(v_t2)};
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -288,18 +305,21 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     auto prepare_loads = [&](int k0, int ke) __attribute__((always_inline)) {
         if (k0 + BN > ke || (k0 & 63) != ld_o) plan_loads(k0, ke);
     };
-    auto issue_one = [&](int i, int k0, unsigned char* kd, unsigned char* vd)
-        __attribute__((always_inline)) {
-        const int blk = (i % NI) * NW + wave;
-        const void* base = i < NI ? static_cast<const void*>(kp + static_cast<int64_t>(k0) * a.k_st)
-                           : VT   ? static_cast<const void*>(vp + static_cast<int64_t>(k0 & ~63) * D)
-                                  : static_cast<const void*>(vp + static_cast<int64_t>(k0) * a.v_st);
-        lds_dma16(uniform_ptr(base), ld_off[i], lds_addr((i < NI ? kd : vd) + blk * 1024));
+    // Loads j of the K tile and of the V tile (0 <= j < NI), one 1 KB LDS block
+    // each, issued together; ldk, ldv are the LDS byte addresses of the tiles.
+    const uint32_t lds_wave = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave * 1024));
+    auto issue_pair = [&](int j, int k0, uint32_t ldk, uint32_t ldv) __attribute__((always_inline)) {
+        const void* kbase = kp + static_cast<int64_t>(k0) * a.k_st;
+        const void* vbase = VT ? static_cast<const void*>(vp + static_cast<int64_t>(k0 & ~63) * D)
+                               : static_cast<const void*>(vp + static_cast<int64_t>(k0) * a.v_st);
+        const uint32_t blk = lds_wave + j * NW * 1024;
+        lds_dma16x2(uniform_ptr(kbase), ld_off[j], ldk + blk, uniform_ptr(vbase), ld_off[NI + j],
+                    ldv + blk);
     };
-    auto issue = [&](int k0, int ke, unsigned char* kd, unsigned char* vd) __attribute__((always_inline)) {
+    auto issue = [&](int k0, int ke, uint32_t ldk, uint32_t ldv) __attribute__((always_inline)) {
         prepare_loads(k0, ke);
 #pragma unroll
-        for (int i = 0; i < 2 * NI; ++i) issue_one(i, k0, kd, vd);
+        for (int j = 0; j < NI; ++j) issue_pair(j, k0, ldk, ldv);
     };
 
     // Q^T operand (B of the S^T MFMA): lane holds q[row][16*kk + 8*hw .. +8].
@@ -346,33 +366,38 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     // no wave stalls on a full load queue while the others also issue theirs.
     constexpr int kAhead = 4;  // LDS operand reads run this many MFMAs ahead
     auto compute = [&](const unsigned char* kb, const unsigned char* vb, int k0, int ke, int nk0,
-                       int nke, unsigned char* nkd, unsigned char* nvd) __attribute__((always_inline)) {
+                       int nke, uint32_t nkd, uint32_t nvd) __attribute__((always_inline)) {
         // ---- S^T = K Q^T: two 32-key blocks x 32 queries per wave
         f32x16_t s0 = f32x16_t{}, s1 = f32x16_t{};
-        constexpr int kLoadEvery = KK / (2 * NI);
-        static_assert(kLoadEvery >= 1 && kLoadEvery * 2 * NI == KK, "loads must spread evenly");
+        constexpr int kLoadEvery = KK / NI;  // k-steps between two load pairs
+        static_assert(kLoadEvery >= 1 && kLoadEvery * NI == KK, "loads must spread evenly");
+        // K fragments are read in batches of four (two k-steps), one batch
+        // ahead; one explicit wait per batch covers its four MFMAs.
         bf16x8_t kf[2 * KK];
+        auto read_k = [&](int bt) __attribute__((always_inline)) {
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            const int off = k_row_off + (((2 * kk + hw) ^ k_swz) << 4);
-            kf[2 * kk] = *reinterpret_cast<const bf16x8_t*>(kb + off);
-            kf[2 * kk + 1] = *reinterpret_cast<const bf16x8_t*>(kb + off + 32 * ROWB);
-        }
+            for (int kk = 2 * bt; kk < 2 * bt + 2; ++kk) {
+                const int off = k_row_off + (((2 * kk + hw) ^ k_swz) << 4);
+                kf[2 * kk] = *reinterpret_cast<const bf16x8_t*>(kb + off);
+                kf[2 * kk + 1] = *reinterpret_cast<const bf16x8_t*>(kb + off + 32 * ROWB);
+            }
+        };
+        constexpr int KB = KK / 2;  // batches
+        read_k(0);
+        if (KB > 1) read_k(1);
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            s0 = mfma32x32x16(kf[2 * kk], qf[kk], s0);
-            s1 = mfma32x32x16(kf[2 * kk + 1], qf[kk], s1);
-            if (kk % kLoadEvery == 0) issue_one(kk / kLoadEvery, nk0, nkd, nvd);
-        }
-        // Each K fragment is read kAhead MFMAs before the MFMA that uses it,
-        // so the LDS latency hides behind the wave's own MFMAs.
-        __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);  // LDS reads
+        for (int bt = 0; bt < KB; ++bt) {
+            if (bt + 1 < KB) wait_lds_reads<4>(); else wait_lds_reads<0>();
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 2 * KK - kAhead; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+            for (int kk = 2 * bt; kk < 2 * bt + 2; ++kk) {
+                s0 = mfma32x32x16(kf[2 * kk], qf[kk], s0);
+                s1 = mfma32x32x16(kf[2 * kk + 1], qf[kk], s1);
+                if (kk % kLoadEvery == 0) issue_pair(kk / kLoadEvery, nk0, nkd, nvd);
+            }
+            if (bt + 2 < KB) read_k(bt + 2);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
 
         // Output layout: register i of a lane holds S^T row 8*(i/4) + 4*hw + i%4,
         // i.e. key 16*(i/8) + 8*hw + i%8 with the permuted K rows.
@@ -441,23 +466,25 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
         if constexpr (VT) {
             // Row 32*d + l32 of the V^T tile, keys 16*j + 8*hw .. + 7, each
             // fragment read kAhead MFMAs before its MFMA.
+            // V fragments in batches of DB (one k-step), one batch ahead, one
+            // explicit wait per batch.
             bf16x8_t vf[4 * DB];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
+            auto read_v = [&](int j) __attribute__((always_inline)) {
 #pragma unroll
                 for (int d = 0; d < DB; ++d)
                     vf[j * DB + d] = *reinterpret_cast<const bf16x8_t*>(vb + vt_off[j] + d * 32 * kVtRowBytes);
+            };
+            read_v(0);
+            read_v(1);
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < 4; ++j) {
+                if (j < 3) wait_lds_reads<DB>(); else wait_lds_reads<0>();
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int d = 0; d < DB; ++d) acc[d] = mfma32x32x16(vf[j * DB + d], pf[j], acc[d]);
-            __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
-#pragma unroll
-            for (int i = 0; i < 4 * DB - kAhead; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                if (j + 2 < 4) read_v(j + 2);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
             return;
         }
 #pragma unroll
@@ -501,15 +528,15 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     for (int r = 0; r < tr.n; ++r) n += (range_end(a, tr, r) - range_begin(a, tr, r) + BN - 1) / BN;
     KeyTile cur{0, range_begin(a, tr, 0), range_end(a, tr, 0)};
     KeyTile ld1 = advance(cur);  // tile t+1
-    issue(cur.k0, cur.ke, kbuf[0], vbuf[0]);
-    issue(ld1.k0, ld1.ke, kbuf[1], vbuf[1]);
+    issue(cur.k0, cur.ke, lds_k[0], lds_v[0]);
+    issue(ld1.k0, ld1.ke, lds_k[1], lds_v[1]);
     KeyTile ld2 = advance(ld1);  // tile t+2
     auto step = [&](int b) __attribute__((always_inline)) {
         prepare_loads(ld2.k0, ld2.ke);
         wait_lds_dma_but<2 * NI>();
         __syncthreads();  // tile t is in buffer b for every wave
         const int bn = b == 0 ? 2 : b - 1;  // (t + 2) % 3
-        compute(kbuf[b], vbuf[b], cur.k0, cur.ke, ld2.k0, ld2.ke, kbuf[bn], vbuf[bn]);
+        compute(kbuf[b], vbuf[b], cur.k0, cur.ke, ld2.k0, ld2.ke, lds_k[bn], lds_v[bn]);
         cur = ld1;
         ld1 = ld2;
         ld2 = advance(ld2);
