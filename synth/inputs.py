@@ -77,6 +77,19 @@ WORKLOADS: dict[str, Workload] = {
                  notes="10 chunks x 2 denoising steps x 40 layers of append + attention"),
         Workload(5, "wan14b_720p_chunk_b2", "bf16", 2, 40, 128, 3600, 3, 1, 1, n_chunks=2,
                  notes="two independent streams, one 10800-query chunk over 25200 keys each"),
+        # Variants the paper reports (parity cases): its deployed 512x512
+        # resolution (32x32 patches per latent frame), 7-frame chunks, a
+        # 720x720 frame (45x45 patches), and a window of two previous chunks
+        # with a three-frame c_0. The last three use 8 heads to keep the
+        # oracle's share of the test time small; heads are independent.
+        Workload(6, "paper_512_chunk", "bf16", 1, 40, 128, 1024, 3, 1, 1, n_chunks=2,
+                 notes="3072 queries over 1024 ref + 3072 previous + 3072 current keys"),
+        Workload(7, "paper_480p_chunk7", "bf16", 1, 8, 128, 1560, 7, 1, 1, n_chunks=2,
+                 notes="7-frame chunks: 10920 queries over 1560 + 10920 + 10920 keys"),
+        Workload(8, "paper_720x720_chunk", "bf16", 1, 8, 128, 2025, 3, 1, 1, n_chunks=2,
+                 notes="6075 queries over 2025 + 6075 + 6075 keys (token counts not multiples of 8)"),
+        Workload(9, "window2_ref3_stream", "bf16", 1, 8, 128, 1560, 3, 3, 2, n_chunks=4,
+                 notes="W = 2 and a 3-frame c_0: chunks 3 and 4 see c_0 + three chunks"),
     ]
 }
 

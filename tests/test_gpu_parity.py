@@ -458,6 +458,36 @@ def test_720p_two_streams_sampled(tm):
     assert_close(from_dev(o)[:, rows][:, :, heads], o_ref, "bf16", "720p b2")
 
 
+VARIANTS = ["paper_512_chunk", "paper_480p_chunk7", "paper_720x720_chunk", "window2_ref3_stream"]
+
+
+@pytest.mark.parametrize("name", VARIANTS)
+def test_paper_variants_streamed_sampled(tm, name):
+    """Shapes the paper also reports (deployed 512x512 resolution, 7-frame
+    chunks, 720x720 frames with token counts that are not multiples of 8, a
+    window of two chunks with a three-frame c_0): streamed through the cache,
+    sampled parity at every chunk from the first that sees the full window."""
+    w = WORKLOADS[name]
+    g = _geom(w)
+    desc = _desc(tm, w)
+    cache = tm.KVCache(desc)
+    hist = StreamHistory(g)
+    heads = [0, w.heads - 1]
+    for t in range(w.n_chunks + 1):
+        dd = draw_chunk(w, t)
+        q, k, v = chunk_to_dev(dd, "bf16")
+        tm.tm_kv_append(cache, t, k, v)
+        hist.append(t, dd["k"], dd["v"])
+        o = tm.tm_sparse_causal_attn_fwd(desc, q, t, cache=cache)
+        if t < min(w.window + 1, w.n_chunks):
+            continue
+        torch.cuda.synchronize()
+        rows = sample_rows(q.shape[1], k=32)
+        o_ref, _ = hist.attend(dd["q"], t, heads=heads, rows=rows)
+        say(f"{name}: chunk {t}, {q.shape[1]} queries, heads {heads}, {len(rows)} rows")
+        assert_close(from_dev(o)[:, rows][:, :, heads], o_ref, "bf16", f"{name} chunk {t}")
+
+
 def test_480p_streaming_loop_two_steps_sampled(tm):
     """The streaming loop at 480p shapes: one cache per denoising step, chunks
     1..3 appended and attended at both steps; sampled parity per (chunk, step)."""
