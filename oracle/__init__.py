@@ -21,6 +21,8 @@ What it computes, and where the paper defines it:
   host (Sec. 4.3, "KV & Embedding Cachings").
 * ``brute``     -- an independent fp64 per-query enumeration of the same key
   set, used to pin ``attention`` on tiny inputs.
+* ``producer``  -- the RMS normalisation of query and key rows that precedes
+  the attention and the KV cache (the fused K/V producer).
 
 Every function here is pinned by the ``-m "not gpu"`` tests against closed
 forms, invariants, library special cases and the brute force; the one reading
@@ -40,3 +42,4 @@ from .attention import (  # noqa: F401
     StreamHistory,
 )
 from .brute import brute_force_attention  # noqa: F401
+from .producer import rms_normalise  # noqa: F401

@@ -330,3 +330,37 @@ def test_synthetic_inputs_are_bf16_exact_and_rms_normalised():
     assert np.array_equal(x, x2)
     d = draw_qkv_sequence(WORKLOADS["tiny_f32"])
     assert d["q"].shape == (1, 9 * 64, 2, 64) and d["q"].dtype == np.float32
+
+
+# --------------------------------------------------------------------------- fused K/V producer
+
+
+def test_rms_normalise_rows_have_unit_rms_and_are_scale_free():
+    from oracle import rms_normalise
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((3, 17, 4, 128)) * rng.uniform(0.1, 10.0, size=(3, 17, 4, 1))
+    y = rms_normalise(x)
+    assert np.allclose(np.sqrt(np.mean(y * y, axis=-1)), 1.0, rtol=0, atol=1e-12)
+    assert np.allclose(rms_normalise(7.5 * x), y, rtol=0, atol=1e-12)  # positive scale drops out
+    assert np.array_equal(np.sign(y), np.sign(x))                      # direction kept per element
+
+
+def test_rms_normalise_gain_and_eps_closed_forms():
+    from oracle import rms_normalise
+    x = np.full((1, 2, 3, 64), 2.0)                       # mean square 4
+    g = np.arange(3 * 64, dtype=np.float64).reshape(3, 64)
+    assert np.allclose(rms_normalise(x, g), g[None, None] * 1.0)             # 2 / sqrt(4) = 1
+    assert np.allclose(rms_normalise(x, None, eps=5.0), 2.0 / 3.0)           # 2 / sqrt(4 + 5)
+    one_hot = np.zeros((1, 1, 1, 128)); one_hot[..., 7] = 3.0                # mean square 9/128
+    assert np.allclose(rms_normalise(one_hot)[..., 7], np.sqrt(128.0))
+
+
+def test_rms_normalise_matches_torch_rms_norm():
+    torch = pytest.importorskip("torch")
+    from oracle import rms_normalise
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal((2, 9, 5, 128))
+    g = rng.uniform(0.5, 1.5, size=(5, 128))
+    for eps in (0.0, 1e-6):
+        ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (128,), eps=eps).numpy() * g
+        assert np.allclose(rms_normalise(x, g, eps), ref, rtol=1e-12, atol=1e-12)

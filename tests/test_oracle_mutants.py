@@ -94,3 +94,49 @@ def _attn_unnormalised(q, k, v, mask, scale, *, dtype=np.float32, return_probs=F
 def test_planted_mistake_is_caught(monkeypatch, target, name, mutant):
     monkeypatch.setattr(target, name, mutant)
     assert not _pins_hold()
+
+
+# --------------------------------------------------------------------------- producer mutants
+
+
+def _producer_pins_hold(fn):
+    """The unit-RMS, closed-form and torch pins of ``test_oracle`` against fn."""
+    import torch
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((2, 5, 3, 64)) * rng.uniform(0.5, 4.0, size=(2, 5, 3, 1))
+    g = rng.uniform(0.5, 1.5, size=(3, 64))
+    y = fn(x)
+    ok = np.allclose(np.sqrt(np.mean(y * y, axis=-1)), 1.0, atol=1e-10)
+    ok &= np.allclose(fn(np.full((1, 1, 3, 64), 2.0), None, eps=5.0), 2.0 / 3.0)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (64,), eps=1e-6).numpy() * g
+    ok &= np.allclose(fn(x, g, 1e-6), ref, atol=1e-10)
+    return bool(ok)
+
+
+def _rms_over_heads(x, gain=None, eps=0.0):
+    x = np.asarray(x, dtype=np.float64)
+    y = x / np.sqrt(np.mean(x * x, axis=(-2, -1), keepdims=True) + eps)  # wrong group
+    return y * gain if gain is not None else y
+
+
+def _rms_eps_outside(x, gain=None, eps=0.0):
+    x = np.asarray(x, dtype=np.float64)
+    y = x / (np.sqrt(np.mean(x * x, axis=-1, keepdims=True)) + eps)  # eps after the root
+    return y * gain if gain is not None else y
+
+
+def _rms_no_root(x, gain=None, eps=0.0):
+    x = np.asarray(x, dtype=np.float64)
+    y = x / (np.mean(x * x, axis=-1, keepdims=True) + eps)  # mean square, not its root
+    return y * gain if gain is not None else y
+
+
+def test_unmutated_producer_oracle_passes():
+    from oracle import rms_normalise
+    assert _producer_pins_hold(rms_normalise)
+
+
+@pytest.mark.parametrize("mutant", [_rms_over_heads, _rms_eps_outside, _rms_no_root],
+                         ids=["group_over_heads", "eps_outside_root", "no_root"])
+def test_producer_mutants_fail_a_pin(mutant):
+    assert not _producer_pins_hold(mutant)
