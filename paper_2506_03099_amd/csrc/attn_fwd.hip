@@ -10,22 +10,26 @@
 //
 // bf16 kernel: one workgroup of 8 waves (two per SIMD) per 256-row query tile,
 // 32 query rows per wave; all 8 waves share each K/V tile staged in LDS.
-// Per 64-key tile:
+// Per 64-key tile the work is
 //   S^T (keys x queries) = K Q^T with v_mfma_f32_32x32x16_bf16, K from LDS,
 //     Q^T held in registers for the whole loop;
-//   online softmax in fp32 on the MFMA output layout, where each lane owns one
-//     query column and half of its keys; exp2 with the scale folded in, and a
-//     lazily-updated running max (the accumulator is only rescaled when the
-//     max grows by more than 2^8, which keeps P <= 256);
+//   the softmax in fp32 on the MFMA output layout (each lane owns one query
+//     column and half of its keys): x = S*scale*log2(e) - m against a lazily
+//     raised running max m, P = exp2(x) rounded to bf16, row sums of that P;
 //   O^T (head_dim x queries) += V^T P^T with the same MFMA, P^T straight from
-//     registers (bf16, rounded to nearest even). From the KV cache, whose V
-//     blocks are stored dimension-major, the V tile lands in LDS as V^T and
-//     each operand is one 16-byte read; the K rows are fed to the S MFMA in a
-//     permuted order that makes each lane's P^T elements 8 consecutive keys.
-//     From row-major V (whole-sequence calls on caller tensors) the operand is
-//     read with the gfx950 transposing LDS read.
-// K/V tiles are double-buffered in LDS and filled by direct global->LDS loads,
-// so the next tile's loads are in flight while the current tile is computed.
+//     registers. From the KV cache, whose V blocks are stored dimension-major,
+//     the V tile lands in LDS as V^T and each operand is one 16-byte read; the
+//     K rows are fed to the S MFMA in a permuted order that makes each lane's
+//     P^T elements 8 consecutive keys. From row-major V (whole-sequence calls
+//     on caller tensors) the operand is read with the gfx950 transposing read.
+// The loop is software-pipelined so that every wave keeps the matrix core fed
+// with its own VALU work in between (a wave's VALU work overlaps the MFMAs of
+// the same wave far better than those of the other wave on its SIMD): while
+// the MFMAs of S(t+1) run, the same wave forms P(t); while those of P(t) V(t)
+// run, it scales S(t+1). Each MFMA is preceded by the LDS read of the operand
+// fragment four MFMAs ahead. K/V tiles stream through four LDS buffers per
+// tensor, filled by direct global->LDS loads two (V) and four (K) tiles ahead,
+// with one barrier per tile.
 //
 // fp32 kernel: a plain VALU kernel (4 lanes per query row, exact running max)
 // for fp32 inputs; it exists for correctness at small sizes.
@@ -44,6 +48,8 @@ typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
 constexpr float kNegInf = -__builtin_inff();
 // Threads per workgroup of the bf16 kernel: 8 waves (two per SIMD) sharing
@@ -51,13 +57,6 @@ constexpr float kNegInf = -__builtin_inff();
 constexpr int kBf16Threads = 512;
 // s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
 constexpr int kWaitVmcnt0 = 0x0F70;
-
-// 32-bit LDS byte address of a __shared__ object, made wave-uniform.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
-        (const __attribute__((address_space(3))) unsigned char*)(p)));
-    return __builtin_amdgcn_readfirstlane(a);
-}
 
 // A pointer that is the same in every lane, held in scalar registers.
 __device__ __forceinline__ const void* uniform_ptr(const void* p) {
@@ -112,6 +111,15 @@ template <int N>
 __device__ __forceinline__ void wait_lds_dma_but() {
     static_assert(N >= 0 && N < 16, "vmcnt field");
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0 | N);
+}
+
+// Keeps x in a register at this point of the program: the empty statement
+// takes x as input and output, so the computation of x cannot be moved past
+// it (the compiler would otherwise sink work that is only used after a branch
+// or a barrier, away from the MFMAs it is meant to overlap).
+__device__ __forceinline__ float pin(float x) {
+    asm volatile("" : "+v"(x));
+    return x;
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
@@ -237,21 +245,26 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     constexpr int CPR = D / 8;         // 16-byte chunks per key row
     constexpr int ROWB = D * 2;        // bytes per key row
     constexpr int TILEB = BN * ROWB;
-    constexpr int NW = kBf16Threads / 64;   // waves per workgroup, 32 query rows each
+    constexpr int NW = kBf16Threads / 64;            // waves per workgroup, 32 query rows each
     constexpr int NI = TILEB / (kBf16Threads * 16);  // direct loads per thread per tensor per tile
-    constexpr int KK = D / 16;              // MFMA k-steps over head_dim
-    constexpr int DB = D / 32;              // 32-row blocks of O^T
+    constexpr int KK = D / 16;  // MFMA k-steps over head_dim
+    constexpr int DB = D / 32;  // 32-row blocks of O^T
+    constexpr int NK = 2 * KK;  // K fragments per tile = score MFMAs per wave
+    constexpr int NV = 4 * DB;  // V fragments per tile = P.V MFMAs per wave
+    constexpr int NF = NK + NV;
+    constexpr int RING = 4;        // fragments read ahead of their MFMA
+    constexpr int EPG = 32 / NK;   // P elements formed per score MFMA
+    constexpr int FPG = 32 / NV;   // scores scaled per P.V MFMA
+    constexpr int NBUF = 4;        // LDS buffers per tensor
     static_assert(NI * kBf16Threads * 16 == TILEB, "tile must split evenly over the threads");
     static_assert(BM == NW * 32, "one 32-row query block per wave");
+    static_assert(NF % RING == 0 && NK >= RING && EPG % 2 == 0, "fragment ring layout");
 
-    // Three K and three V tiles, each its own LDS object so that the compiler
-    // can tell a tile being read from the tiles whose loads are in flight.
-    __shared__ __attribute__((aligned(1024))) unsigned char k_t0[TILEB], k_t1[TILEB], k_t2[TILEB];
-    __shared__ __attribute__((aligned(1024))) unsigned char v_t0[TILEB], v_t1[TILEB], v_t2[TILEB];
-    unsigned char* const kbuf[3] = {k_t0, k_t1, k_t2};
-    unsigned char* const vbuf[3] = {v_t0, v_t1, v_t2};
-    const uint32_t lds_k[3] = {lds_addr(k_t0), lds_addr(k_t1), lds_addr(k_t2)};
-    const uint32_t lds_v[3] = {lds_addr(v_t0), lds_addr(v_t1), lds_addr(v_t2)};
+    // K tile j sits in buffer j % 4 of the first four, V tile j in buffer
+    // j % 4 of the last four.
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * NBUF * TILEB];
+    lds_u8* const L = (lds_u8*)(smem);
+    const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(L));
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -271,58 +284,80 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     const __bf16* kp = static_cast<const __bf16*>(a.k) + bat * a.k_sb + head * a.k_sh;
     const __bf16* vp = static_cast<const __bf16*>(a.v) + bat * a.v_sb + head * a.v_sh;
 
-    // Issue the direct loads of one K tile and one V tile. Rows past the range
-    // end re-read the range's last row (finite data; its scores are masked).
-    // A V^T tile takes, for each dimension d, the 8-key groups of the tile from
-    // the cache's V block(s); groups past the range end re-read the group that
-    // holds the range's last key (its other columns are the append's zeros).
-    // This wave's share of one tile's direct loads: 2 * NI loads of one 1 KB
-    // LDS block each, the first NI for the K tile, the rest for the V tile.
-    // Lane offsets from the tile's scalar bases are kept in ld_off; they only
-    // change with k0 mod 64 (V^T) or for a range's last tile (rows past the
-    // range end re-read its last row, V^T groups past it the group holding
-    // its last key), so plan_loads recomputes them only then.
-    uint32_t ld_off[2 * NI];
-    int ld_o = -1;  // k0 mod 64 that ld_off was planned for; -1 after a last tile
-    auto plan_loads = [&](int k0, int ke) __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < 2 * NI; ++i) {
-            const int ch = ((i % NI) * NW + wave) * 64 + lane;
-            if (i < NI || !VT) {
-                const int row = min(ch / CPR, ke - 1 - k0);
-                const int gc = (ch % CPR) ^ lds_swizzle<D>(ch / CPR);
-                const int64_t st = i < NI ? a.k_st : a.v_st;
-                ld_off[i] = static_cast<uint32_t>((row * st + gc * 8) * 2);
-            } else {
-                const int d = ch >> 3;
-                const int b0 = k0 & ~63;  // first cache block of the tile
-                const int g = min(k0 + 8 * ((ch & 7) ^ vt_swizzle(d)), (ke - 1) & ~7) - b0;
-                ld_off[i] = static_cast<uint32_t>(((g >> 6) * (64 * D) + d * 64 + (g & 63)) * 2);
-            }
+    // ---- key tiles: the tiles of range 0, then those of range 1, ... Tile j
+    // of the walk (clamped to the last tile) is found by counting tiles per
+    // range; this runs only at range boundaries.
+    struct KeyTile {
+        int k0, ke;
+    };
+    auto range_tiles = [&](int r) { return (range_end(a, tr, r) - range_begin(a, tr, r) + BN - 1) / BN; };
+    int n = 0;
+    for (int r = 0; r < tr.n; ++r) n += range_tiles(r);
+    auto tile_at = [&](int j) __attribute__((always_inline)) {
+        j = min(j, n - 1);
+        int r = 0, first = 0;
+        while (r + 1 < tr.n && j >= first + range_tiles(r)) {
+            first += range_tiles(r);
+            ++r;
         }
-        ld_o = k0 + BN <= ke ? (k0 & 63) : -1;
+        return KeyTile{range_begin(a, tr, r) + (j - first) * BN, range_end(a, tr, r)};
     };
-    auto prepare_loads = [&](int k0, int ke) __attribute__((always_inline)) {
-        if (k0 + BN > ke || (k0 & 63) != ld_o) plan_loads(k0, ke);
-    };
-    // Loads j of the K tile and of the V tile (0 <= j < NI), one 1 KB LDS block
-    // each, issued together; ldk, ldv are the LDS byte addresses of the tiles.
-    const uint32_t lds_wave = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave * 1024));
-    auto issue_pair = [&](int j, int k0, uint32_t ldk, uint32_t ldv) __attribute__((always_inline)) {
-        const void* kbase = kp + static_cast<int64_t>(k0) * a.k_st;
-        const void* vbase = VT ? static_cast<const void*>(vp + static_cast<int64_t>(k0 & ~63) * D)
-                               : static_cast<const void*>(vp + static_cast<int64_t>(k0) * a.v_st);
-        const uint32_t blk = lds_wave + j * NW * 1024;
-        lds_dma16x2(uniform_ptr(kbase), ld_off[j], ldk + blk, uniform_ptr(vbase), ld_off[NI + j],
-                    ldv + blk);
-    };
-    auto issue = [&](int k0, int ke, uint32_t ldk, uint32_t ldv) __attribute__((always_inline)) {
-        prepare_loads(k0, ke);
-#pragma unroll
-        for (int j = 0; j < NI; ++j) issue_pair(j, k0, ldk, ldv);
+    // Smallest tile index >= j whose tile ends its range (the walk's last
+    // tile if there is none).
+    auto next_range_end = [&](int j) __attribute__((always_inline)) {
+        int last = 0;
+        for (int r = 0; r < tr.n; ++r) {
+            last += range_tiles(r);
+            if (last - 1 >= j) return last - 1;
+        }
+        return n - 1;
     };
 
-    // Q^T operand (B of the S^T MFMA): lane holds q[row][16*kk + 8*hw .. +8].
+    // ---- direct global->LDS loads of one tile. Rows past the range end
+    // re-read the range's last row (finite data; its scores are masked). A V^T
+    // tile takes, for each dimension d, the 8-key groups of the tile from the
+    // cache's V block(s); groups past the range end re-read the group holding
+    // the range's last key (its other columns are the append's zeros). Each
+    // wave loads NI blocks of 1 KB per tensor. The lane offsets from the
+    // tile's scalar base are the same for every tile of a range except its
+    // last, so they are planned again only for a range's last tile and for the
+    // tile after it.
+    auto plan = [&](uint32_t (&off)[NI], bool is_v, const KeyTile& t) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int ch = (i * NW + wave) * 64 + lane;
+            if (!is_v || !VT) {
+                const int row = min(ch / CPR, t.ke - 1 - t.k0);
+                const int gc = (ch % CPR) ^ lds_swizzle<D>(ch / CPR);
+                const int64_t st = is_v ? a.v_st : a.k_st;
+                off[i] = static_cast<uint32_t>((row * st + gc * 8) * 2);
+            } else {
+                const int d = ch >> 3;
+                const int b0 = t.k0 & ~63;  // first cache block of the tile
+                const int g = min(t.k0 + 8 * ((ch & 7) ^ vt_swizzle(d)), (t.ke - 1) & ~7) - b0;
+                off[i] = static_cast<uint32_t>(((g >> 6) * (64 * D) + d * 64 + (g & 63)) * 2);
+            }
+        }
+    };
+    const uint32_t lds_wave = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave * 1024));
+    // Byte offsets of K buffer j % 4 from the start of LDS, and of V buffer
+    // j % 4 from the start of the V buffers (NBUF * TILEB further on).
+    auto kbuf = [](int j) { return static_cast<uint32_t>((j % NBUF) * TILEB); };
+    auto vbuf = [](int j) { return static_cast<uint32_t>((j % NBUF) * TILEB); };
+    auto kbase = [&](const KeyTile& t) { return uniform_ptr(kp + static_cast<int64_t>(t.k0) * a.k_st); };
+    auto vbase = [&](const KeyTile& t) {
+        return VT ? uniform_ptr(vp + static_cast<int64_t>(t.k0 & ~63) * D)
+                  : uniform_ptr(vp + static_cast<int64_t>(t.k0) * a.v_st);
+    };
+    // Load i (0 <= i < NI) of two tiles issued together: source p0 + lane
+    // offset o0 into LDS byte offset l0, and likewise p1, o1, l1.
+    auto dma_pair = [&](int i, const void* p0, uint32_t o0, uint32_t l0, const void* p1, uint32_t o1,
+                        uint32_t l1) __attribute__((always_inline)) {
+        const uint32_t blk = lds_base + lds_wave + i * NW * 1024;
+        lds_dma16x2(p0, o0, l0 + blk, p1, o1, l1 + blk);
+    };
+
+    // ---- Q^T operand (B of the score MFMA): lane holds q[row][16*kk + 8*hw .. +8].
     const int qrow = tr.q0 + wave * 32 + l32;
     const bool row_ok = qrow < tr.q1;
     bf16x8_t qf[KK];
@@ -338,215 +373,257 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     // compiler places for them can be miscounted.
     wait_lds_dma();
 
-    f32x16_t acc[DB];
-#pragma unroll
-    for (int i = 0; i < DB; ++i) acc[i] = f32x16_t{};
-    float m_run = kNegInf;  // running max in the scaled log2 domain
-    float l_run = 0.f;      // this lane's partial row sum (its 32 keys per tile)
-    const float c = a.scale_log2;
-
-    // Per-lane LDS byte offsets. K operand: row l32 (and l32 + 32), chunk
-    // 2*kk + hw. V^T operand via the transposing read: rows 16*j + 4*hw + gi/4
-    // (and + 8), element columns 32*d + 16*(grp & 1) + 4*(gi & 3).
+    // ---- per-lane LDS byte offsets of the operand fragments within a tile.
+    // K fragment (kk, kb): row l32 + 32*kb (permuted with VT), chunk 2*kk + hw.
     const int k_row = VT ? k_perm(l32) : l32;
-    const int k_row_off = k_row * ROWB;
     const int k_swz = lds_swizzle<D>(k_row);
+    uint32_t koff[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) koff[kk] = k_row * ROWB + (((2 * kk + hw) ^ k_swz) << 4);
+    // V fragment (j, d): with VT, row 32*d + l32 of the V^T tile, keys
+    // 16*j + 8*hw .. + 7; else two transposing reads of the row-major tile,
+    // rows 16*j + 4*hw + gi/4 (and + 8), element columns 32*d + 16*(grp & 1) +
+    // 4*(gi & 3).
+    constexpr int kVtRowBytes = 64 * 2;  // a V^T row: 64 keys
     const int grp = lane >> 4, gi = lane & 15;
     const int v_row = 4 * hw + (gi >> 2);
     const int v_swz_lo = lds_swizzle<D>(v_row), v_swz_hi = lds_swizzle<D>(v_row + 8);
     const int v_cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
     const int v_half = (gi & 1) * 8;
-    constexpr int kVtRowBytes = 64 * 2;  // a V^T row: 64 keys
-    int vt_off[4];
+    uint32_t voff[VT ? 4 : 2 * DB];
+    if constexpr (VT) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) vt_off[j] = l32 * kVtRowBytes + (((2 * j + hw) ^ vt_swizzle(l32)) << 4);
-
-    // One tile: keys [k0, ke) from buffers kb, vb. The loads of the next tile
-    // (keys from nk0 into nkd, nvd) are spread over the score MFMAs, so that
-    // no wave stalls on a full load queue while the others also issue theirs.
-    constexpr int kAhead = 4;  // LDS operand reads run this many MFMAs ahead
-    auto compute = [&](const unsigned char* kb, const unsigned char* vb, int k0, int ke, int nk0,
-                       int nke, uint32_t nkd, uint32_t nvd) __attribute__((always_inline)) {
-        // ---- S^T = K Q^T: two 32-key blocks x 32 queries per wave
-        f32x16_t s0 = f32x16_t{}, s1 = f32x16_t{};
-        constexpr int kLoadEvery = KK / NI;  // k-steps between two load pairs
-        static_assert(kLoadEvery >= 1 && kLoadEvery * NI == KK, "loads must spread evenly");
-        // K fragments are read in batches of four (two k-steps), one batch
-        // ahead; one explicit wait per batch covers its four MFMAs.
-        bf16x8_t kf[2 * KK];
-        auto read_k = [&](int bt) __attribute__((always_inline)) {
+        for (int j = 0; j < 4; ++j)
+            voff[j] = NBUF * TILEB + l32 * kVtRowBytes + (((2 * j + hw) ^ vt_swizzle(l32)) << 4);
+    } else {
 #pragma unroll
-            for (int kk = 2 * bt; kk < 2 * bt + 2; ++kk) {
-                const int off = k_row_off + (((2 * kk + hw) ^ k_swz) << 4);
-                kf[2 * kk] = *reinterpret_cast<const bf16x8_t*>(kb + off);
-                kf[2 * kk + 1] = *reinterpret_cast<const bf16x8_t*>(kb + off + 32 * ROWB);
-            }
-        };
-        constexpr int KB = KK / 2;  // batches
-        read_k(0);
-        if (KB > 1) read_k(1);
-#pragma unroll
-        for (int bt = 0; bt < KB; ++bt) {
-            if (bt + 1 < KB) wait_lds_reads<4>(); else wait_lds_reads<0>();
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int kk = 2 * bt; kk < 2 * bt + 2; ++kk) {
-                s0 = mfma32x32x16(kf[2 * kk], qf[kk], s0);
-                s1 = mfma32x32x16(kf[2 * kk + 1], qf[kk], s1);
-                if (kk % kLoadEvery == 0) issue_pair(kk / kLoadEvery, nk0, nkd, nvd);
-            }
-            if (bt + 2 < KB) read_k(bt + 2);
-            __builtin_amdgcn_sched_barrier(0);
+        for (int d = 0; d < DB; ++d) {
+            const int cc = 4 * d + v_cbase;
+            voff[2 * d] = NBUF * TILEB + v_row * ROWB + ((cc ^ v_swz_lo) << 4) + v_half;
+            voff[2 * d + 1] = NBUF * TILEB + (v_row + 8) * ROWB + ((cc ^ v_swz_hi) << 4) + v_half;
         }
-
-        // Output layout: register i of a lane holds S^T row 8*(i/4) + 4*hw + i%4,
-        // i.e. key 16*(i/8) + 8*hw + i%8 with the permuted K rows.
-        if (k0 + BN > ke) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int kr = k0 + (VT ? 16 * (i / 8) + 8 * hw + (i % 8)
-                                        : 8 * (i / 4) + 4 * hw + (i % 4));
-                if (kr >= ke) s0[i] = kNegInf;
-                if (kr + 32 >= ke) s1[i] = kNegInf;
+    }
+    // Fragment s of a tile's stream: K fragments 0..NK-1 (kk = s/2, kb = s%2)
+    // from the K buffer at byte offset kb_off, then V fragments
+    // (j = (s-NK)/DB, d = (s-NK)%DB) from the V buffer at vb_off. Lane offset
+    // plus a constant: the buffer offsets fold into the read's immediate.
+    auto read_frag = [&](int s, uint32_t kb_off, uint32_t vb_off) __attribute__((always_inline)) {
+        bf16x8_t f;
+        if (s < NK) {
+            const int kk = s >> 1, kb = s & 1;
+            f = *reinterpret_cast<const lds_bf16x8_t*>(L + koff[kk] + (kb_off + kb * 32 * ROWB));
+        } else {
+            const int j = (s - NK) / DB, d = (s - NK) % DB;
+            if constexpr (VT) {
+                f = *reinterpret_cast<const lds_bf16x8_t*>(L + voff[j] + (vb_off + d * 32 * kVtRowBytes));
+            } else {
+                const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (lds_bf16x4_t*)(L + voff[2 * d] + (vb_off + 16 * j * ROWB)));
+                const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (lds_bf16x4_t*)(L + voff[2 * d + 1] + (vb_off + 16 * j * ROWB)));
+                f = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             }
         }
+        return f;
+    };
 
-        // ---- online softmax against the running max m_run, which is shared
-        // by the two half-waves holding a query's scores. The common path takes
-        // no maximum: P = exp2(S * c - m_run) is formed against the current
-        // m_run and kept unless some lane's sum of its 32 values exceeds 2^16
-        // (or is not finite), i.e. unless a score exceeds m_run by more than 16
-        // in the log2 domain. Otherwise (always on the first tile, rarely
-        // after) the exact maximum of both halves is taken, O and the row sum
-        // are rescaled and P is formed again. P is at most 2^16 either way, so
-        // it and O keep their full relative precision far from overflow.
+    // ---- state
+    f32x16_t acc[DB];
+#pragma unroll
+    for (int i = 0; i < DB; ++i) acc[i] = f32x16_t{};
+    float m_run;            // running max in the scaled log2 domain (lazy)
+    float l_run = 0.f;      // this lane's partial row sum
+    const float c = a.scale_log2;
+    const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+    // S^T output layout: register i of block kb holds key 32*kb + (VT ?
+    // 16*(i/8) + 8*hw + i%8 : 8*(i/4) + 4*hw + i%4) of the tile, query l32.
+    auto key_of = [&](int kb, int i) {
+        return 32 * kb + (VT ? 16 * (i / 8) + 8 * hw + (i % 8) : 8 * (i / 4) + 4 * hw + (i % 4));
+    };
+    auto mask_tile = [&](f32x16_t (&s)[2], const KeyTile& kt) __attribute__((always_inline)) {
+        if (kt.k0 + BN > kt.ke) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    if (kt.k0 + key_of(kb, i) >= kt.ke) s[kb][i] = kNegInf;
+        }
+    };
+    // Largest score of this query in the tile (both half-waves).
+    auto row_max = [&](const f32x16_t (&s)[2]) __attribute__((always_inline)) {
+        float mx = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, fmaxf(s[0][i], s[1][i]));
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    };
+    // P = exp2(x) for elements [e, e + 2) of x, rounded to bf16 into its P^T
+    // operand slot (k-step e/8, slot e%8), summed into *lt.
+    auto form_p2 = [&](const f32x16_t (&x)[2], bf16x8_t (&pf)[4], int e, float& lt) __attribute__((always_inline)) {
+        const float p0 = __builtin_amdgcn_exp2f(x[e >> 4][e & 15]);
+        const float p1 = __builtin_amdgcn_exp2f(x[(e + 1) >> 4][(e + 1) & 15]);
+        pf[e >> 3][e & 7] = static_cast<__bf16>(p0);
+        pf[e >> 3][(e & 7) + 1] = static_cast<__bf16>(p1);
+        const bf16x2_t pp = {pf[e >> 3][e & 7], pf[e >> 3][(e & 7) + 1]};
+        lt = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lt, false);
+    };
+
+    // ---- prologue: tiles 0..3 of K and 0..1 of V in flight, S(0) and its
+    // exact maximum (the lazy running max starts from it), x(0) = S(0)*c - m.
+    uint32_t offk[NI], offv[NI];  // lane offsets of the loads of the current K and V tiles
+    {
+        const KeyTile k0t = tile_at(0), k1t = tile_at(1), k2t = tile_at(2), k3t = tile_at(3);
+        uint32_t o0[NI], o1[NI];
+        plan(o0, false, k0t);
+        plan(o1, true, k0t);
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+            dma_pair(i, kbase(k0t), o0[i], kbuf(0), vbase(k0t), o1[i], NBUF * TILEB + vbuf(0));
+        plan(o0, false, k1t);
+        plan(o1, true, k1t);
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+            dma_pair(i, kbase(k1t), o0[i], kbuf(1), vbase(k1t), o1[i], NBUF * TILEB + vbuf(1));
+        plan(o0, false, k2t);
+        plan(o1, false, k3t);
+#pragma unroll
+        for (int i = 0; i < NI; ++i) dma_pair(i, kbase(k2t), o0[i], kbuf(2), kbase(k3t), o1[i], kbuf(3));
+    }
+    wait_lds_dma();
+    __syncthreads();
+
+    // A wave whose 32 query rows all lie past the tile's end (the last query
+    // tile of a chunk) takes part in the loads and barriers only.
+    const bool busy = __builtin_amdgcn_readfirstlane(static_cast<int>(tr.q0 + wave * 32 < tr.q1)) != 0;
+    f32x16_t xa[2], xb[2];  // x(t) and S(t+1) / x(t+1), alternating roles
+    m_run = 0.f;
+    if (busy) {
+        bf16x8_t kf[NK];
+#pragma unroll
+        for (int s = 0; s < NK; ++s) kf[s] = read_frag(s, kbuf(0), vbuf(0));
+        xa[0] = xa[1] = f32x16_t{};
+#pragma unroll
+        for (int s = 0; s < NK; ++s) xa[s & 1] = mfma32x32x16(kf[s], qf[s >> 1], xa[s & 1]);
+        mask_tile(xa, tile_at(0));
+        m_run = row_max(xa) * c;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) xa[kb][i] = fmaf(xa[kb][i], c, -m_run);
+    }
+    bf16x8_t fr[RING];
+#pragma unroll
+    for (int s = 0; s < RING; ++s) fr[s] = read_frag(s, kbuf(1), vbuf(1));
+
+    // ---- main loop: iteration t, with x = x(t) and nx receiving S(t+1).
+    // Stage 1: the score MFMAs of tile t+1, each with its share of P(t)
+    // (exp2, bf16, row sum). Check: if some lane's row sum of the tile
+    // exceeds 2^16 (a score more than 16 above the running max in the log2
+    // domain, or a non-finite value), raise the max to the tile's maximum,
+    // rescale O and the row sum, and form P(t) again. Stage 2: the P.V MFMAs
+    // of tile t, each with its share of x(t+1) = S(t+1)*c - m. Every MFMA is
+    // preceded by the LDS read of the fragment RING MFMAs ahead; tile t+4 of
+    // K and tile t+2 of V are loaded during stage 2. At the end each wave
+    // waits for its loads of the previous iteration and the barrier publishes
+    // K(t+2), K(t+3) and V(t+1).
+    //
+    // Tiles t+1 (scores), t+2 (V load) and t+4 (K load) move one tile on in
+    // their range unless a tile among t+1..t+4 ends a range; only then (at
+    // most a few iterations per range, and at the end of the walk) are they
+    // looked up afresh, the load offsets planned again and the mask of tile
+    // t+1 decided.
+    int event = 0;                 // smallest range-ending tile index >= the last refresh's t + 2
+    const void* kptr = nullptr;    // K source of tile t+4
+    const void* vptr = nullptr;    // V source of tile t+2
+    KeyTile ks{0, BN};             // tile t+1 when it ends its range (scores to mask)
+    bool mask_next = false;
+    const int64_t kstep = static_cast<int64_t>(BN) * a.k_st * 2;  // bytes per tile of keys
+    const int64_t vstep = static_cast<int64_t>(BN) * (VT ? D : a.v_st) * 2;
+    auto iteration = [&](int u, int t, f32x16_t (&x)[2], f32x16_t (&nx)[2]) __attribute__((always_inline)) {
+        const uint32_t kb1 = kbuf(u + 1), kb2 = kbuf(u + 2), vb0 = vbuf(u);
+        if (__builtin_expect(t + 4 >= event, 0)) {
+            const KeyTile k4 = tile_at(t + 4), v2 = tile_at(t + 2);
+            ks = tile_at(t + 1);
+            mask_next = ks.k0 + BN > ks.ke;
+            plan(offk, false, k4);
+            plan(offv, true, v2);
+            kptr = kbase(k4);
+            vptr = vbase(v2);
+            event = next_range_end(t + 2);
+            // The range bounds may come from scalar loads, which share a
+            // counter with the LDS reads and complete out of order: wait for
+            // them here, on this rare path, so that no full wait lands on the
+            // common path where fragment reads are still in flight.
+            wait_lds_reads<0>();
+        } else {
+            kptr = static_cast<const char*>(kptr) + kstep;
+            vptr = static_cast<const char*>(vptr) + vstep;
+            mask_next = false;
+        }
+        if (!busy) {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) dma_pair(i, kptr, offk[i], kbuf(u), vptr, offv[i], NBUF * TILEB + vbuf(u + 2));
+        } else {
         bf16x8_t pf[4];
-        const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
-        auto form_p = [&](float neg_m) __attribute__((always_inline)) -> float {
+        float lt0 = 0.f, lt1 = 0.f;
+        nx[0] = nx[1] = f32x16_t{};
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                pf[i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s0[i], c, neg_m)));
-                pf[2 + i / 8][i % 8] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s1[i], c, neg_m)));
-            }
-            // Row sum of the bf16-rounded P that is multiplied into V.
-            float l = 0.f;
+        for (int g = 0; g < NK; ++g) {
+            nx[g & 1] = mfma32x32x16(fr[g % RING], qf[g >> 1], nx[g & 1]);
+            fr[g % RING] = read_frag(g + RING, kb1, vb0);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const bf16x2_t pp = {pf[j][2 * e], pf[j][2 * e + 1]};
-                    l = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l, false);
-                }
-            }
-            return l;
-        };
-        float lt = form_p(-m_run);
-        if (__any(!(lt <= 0x1p16f))) {
-            float mx = s0[0];
-#pragma unroll
-            for (int i = 1; i < 16; ++i) mx = fmaxf(mx, s0[i]);
-#pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s1[i]);
-            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx),
-                                                             __float_as_uint(mx), false, false);
-            mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // both halves
-            const float m_new = fmaxf(m_run, mx * c);
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-            m_run = m_new;
+            for (int e = EPG * g; e < EPG * (g + 1); e += 2) form_p2(x, pf, e, (e & 2) ? lt1 : lt0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (__builtin_expect(__any(!(lt0 + lt1 <= 0x1p16f)), 0)) {
+            const float dm = fmaxf(row_max(x), 0.f);
+            const float alpha = __builtin_amdgcn_exp2f(-dm);
+            m_run += dm;
             l_run *= alpha;
 #pragma unroll
             for (int d = 0; d < DB; ++d) acc[d] *= alpha;
-            lt = form_p(-m_run);
+            lt0 = lt1 = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) x[kb][i] -= dm;
+#pragma unroll
+            for (int e = 0; e < 32; e += 2) form_p2(x, pf, e, (e & 2) ? lt1 : lt0);
         }
-        l_run += lt;
-
-        // ---- O^T += V^T P^T. P^T k-step j covers S rows 16*j .. 16*j + 15
-        // with slot e <-> row 16*j + 4*hw + e (e < 4) or 16*j + 8 + 4*hw + e - 4
-        // (e >= 4); the V^T operand reads the same keys, 4 at a time.
-        if constexpr (VT) {
-            // Row 32*d + l32 of the V^T tile, keys 16*j + 8*hw .. + 7, each
-            // fragment read kAhead MFMAs before its MFMA.
-            // V fragments in batches of DB (one k-step), one batch ahead, one
-            // explicit wait per batch.
-            bf16x8_t vf[4 * DB];
-            auto read_v = [&](int j) __attribute__((always_inline)) {
+        l_run += lt0 + lt1;
+        if (mask_next) mask_tile(nx, ks);
+        const float nm = -m_run;
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int d = 0; d < DB; ++d)
-                    vf[j * DB + d] = *reinterpret_cast<const bf16x8_t*>(vb + vt_off[j] + d * 32 * kVtRowBytes);
-            };
-            read_v(0);
-            read_v(1);
+        for (int k = 0; k < NV; ++k) {
+            acc[k % DB] = mfma32x32x16(fr[(NK + k) % RING], pf[k / DB], acc[k % DB]);
+            fr[(NK + k) % RING] = read_frag((NK + k + RING) % NF, NK + k + RING < NF ? kb1 : kb2, vb0);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (j < 3) wait_lds_reads<DB>(); else wait_lds_reads<0>();
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int d = 0; d < DB; ++d) acc[d] = mfma32x32x16(vf[j * DB + d], pf[j], acc[d]);
-                if (j + 2 < 4) read_v(j + 2);
-                __builtin_amdgcn_sched_barrier(0);
+            for (int e = FPG * k; e < FPG * (k + 1); ++e) nx[e >> 4][e & 15] = pin(fmaf(nx[e >> 4][e & 15], c, nm));
+            if (k % (NV / NI) == NV / (2 * NI)) {
+                const int i = k / (NV / NI);
+                dma_pair(i, kptr, offk[i], kbuf(u), vptr, offv[i], NBUF * TILEB + vbuf(u + 2));
             }
-            return;
+            __builtin_amdgcn_sched_barrier(0);
         }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-#pragma unroll
-            for (int d = 0; d < DB; ++d) {
-                const int cc = 4 * d + v_cbase;
-                const int lo = (16 * j + v_row) * ROWB + ((cc ^ v_swz_lo) << 4) + v_half;
-                const int hi = (16 * j + v_row + 8) * ROWB + ((cc ^ v_swz_hi) << 4) + v_half;
-                const bf16x4_t vlo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(vb + lo));
-                const bf16x4_t vhi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(vb + hi));
-                const bf16x8_t vf = __builtin_shufflevector(vlo, vhi, 0, 1, 2, 3, 4, 5, 6, 7);
-                acc[d] = mfma32x32x16(vf, pf[j], acc[d]);
-            }
         }
-    };
-
-    // Triple-buffered main loop, unrolled by three so each buffer is named
-    // statically: tile t sits in buffer t % 3 and is computed while tiles t+1
-    // and t+2 load (the loads of tile t+2 are issued during tile t, into the
-    // buffer of tile t-1, which every wave finished before the barrier at the
-    // top of iteration t). Past the last tile the loads re-read the last tile
-    // (harmless; no one reads those buffers again), which keeps the code free
-    // of branches. Each wave issues 2 * NI loads per tile, so waiting until
-    // at most 2 * NI are outstanding leaves only tile t+1's in flight.
-    struct KeyTile {
-        int r, k0, ke;
-    };
-    auto advance = [&](KeyTile t) __attribute__((always_inline)) {
-        KeyTile u = t;
-        u.k0 += BN;
-        if (u.k0 >= u.ke) {
-            if (u.r + 1 >= tr.n) return t;  // past the end: stay on the last tile
-            u.r += 1;
-            u.k0 = range_begin(a, tr, u.r);
-            u.ke = range_end(a, tr, u.r);
-        }
-        return u;
-    };
-    int n = 0;
-    for (int r = 0; r < tr.n; ++r) n += (range_end(a, tr, r) - range_begin(a, tr, r) + BN - 1) / BN;
-    KeyTile cur{0, range_begin(a, tr, 0), range_end(a, tr, 0)};
-    KeyTile ld1 = advance(cur);  // tile t+1
-    issue(cur.k0, cur.ke, lds_k[0], lds_v[0]);
-    issue(ld1.k0, ld1.ke, lds_k[1], lds_v[1]);
-    KeyTile ld2 = advance(ld1);  // tile t+2
-    auto step = [&](int b) __attribute__((always_inline)) {
-        prepare_loads(ld2.k0, ld2.ke);
+        // The barrier orders only this workgroup's LDS use: the compiler may
+        // not move LDS accesses across it, and no wait is needed for the
+        // fragment reads still in flight (their buffer is not written next).
         wait_lds_dma_but<2 * NI>();
-        __syncthreads();  // tile t is in buffer b for every wave
-        const int bn = b == 0 ? 2 : b - 1;  // (t + 2) % 3
-        compute(kbuf[b], vbuf[b], cur.k0, cur.ke, ld2.k0, ld2.ke, lds_k[bn], lds_v[bn]);
-        cur = ld1;
-        ld1 = ld2;
-        ld2 = advance(ld2);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
     };
-    for (int t = 0; t < n; t += 3) {
-        step(0);
+    for (int t = 0; t < n; t += 4) {
+        iteration(0, t, xa, xb);
         if (t + 1 >= n) break;
-        step(1);
+        iteration(1, t + 1, xb, xa);
         if (t + 2 >= n) break;
-        step(2);
+        iteration(2, t + 2, xa, xb);
+        if (t + 3 >= n) break;
+        iteration(3, t + 3, xb, xa);
     }
     wait_lds_dma();  // no load may still be writing LDS when the workgroup ends
 
