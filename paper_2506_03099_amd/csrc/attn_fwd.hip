@@ -255,7 +255,7 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     constexpr int RING = 4;        // fragments read ahead of their MFMA
     constexpr int EPG = 32 / NK;   // P elements formed per score MFMA
     constexpr int FPG = 32 / NV;   // scores scaled per P.V MFMA
-    constexpr int NBUF = 4;        // LDS buffers per tensor
+    constexpr int NBUF = 4;        // LDS buffers per tensor (a power of two)
     static_assert(NI * kBf16Threads * 16 == TILEB, "tile must split evenly over the threads");
     static_assert(BM == NW * 32, "one 32-row query block per wave");
     static_assert(NF % RING == 0 && NK >= RING && EPG % 2 == 0, "fragment ring layout");
@@ -342,8 +342,8 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     const uint32_t lds_wave = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave * 1024));
     // Byte offsets of K buffer j % 4 from the start of LDS, and of V buffer
     // j % 4 from the start of the V buffers (NBUF * TILEB further on).
-    auto kbuf = [](int j) { return static_cast<uint32_t>((j % NBUF) * TILEB); };
-    auto vbuf = [](int j) { return static_cast<uint32_t>((j % NBUF) * TILEB); };
+    auto kbuf = [](int j) { return static_cast<uint32_t>((j & (NBUF - 1)) * TILEB); };
+    auto vbuf = [](int j) { return static_cast<uint32_t>((j & (NBUF - 1)) * TILEB); };
     auto kbase = [&](const KeyTile& t) { return uniform_ptr(kp + static_cast<int64_t>(t.k0) * a.k_st); };
     auto vbase = [&](const KeyTile& t) {
         return VT ? uniform_ptr(vp + static_cast<int64_t>(t.k0 & ~63) * D)
@@ -539,8 +539,7 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     bool mask_next = false;
     const int64_t kstep = static_cast<int64_t>(BN) * a.k_st * 2;  // bytes per tile of keys
     const int64_t vstep = static_cast<int64_t>(BN) * (VT ? D : a.v_st) * 2;
-    auto iteration = [&](int u, int t, f32x16_t (&x)[2], f32x16_t (&nx)[2]) __attribute__((always_inline)) {
-        const uint32_t kb1 = kbuf(u + 1), kb2 = kbuf(u + 2), vb0 = vbuf(u);
+    auto refresh = [&](int t) __attribute__((always_inline)) {
         if (__builtin_expect(t + 4 >= event, 0)) {
             const KeyTile k4 = tile_at(t + 4), v2 = tile_at(t + 2);
             ks = tile_at(t + 1);
@@ -549,7 +548,7 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             plan(offv, true, v2);
             kptr = kbase(k4);
             vptr = vbase(v2);
-            event = next_range_end(t + 2);
+            event = __builtin_amdgcn_readfirstlane(next_range_end(t + 2));
             // The range bounds may come from scalar loads, which share a
             // counter with the LDS reads and complete out of order: wait for
             // them here, on this rare path, so that no full wait lands on the
@@ -560,10 +559,19 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             vptr = static_cast<const char*>(vptr) + vstep;
             mask_next = false;
         }
-        if (!busy) {
-#pragma unroll
-            for (int i = 0; i < NI; ++i) dma_pair(i, kptr, offk[i], kbuf(u), vptr, offv[i], NBUF * TILEB + vbuf(u + 2));
-        } else {
+    };
+    // The barrier orders only this workgroup's LDS use: the compiler may not
+    // move LDS accesses across it, and no wait is needed for the fragment
+    // reads still in flight (their buffer is not written next).
+    auto end_tile = [&]() __attribute__((always_inline)) {
+        wait_lds_dma_but<2 * NI>();
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    auto iteration = [&](int u, int t, f32x16_t (&x)[2], f32x16_t (&nx)[2]) __attribute__((always_inline)) {
+        const uint32_t kb1 = kbuf(u + 1), kb2 = kbuf(u + 2), vb0 = vbuf(u);
+        refresh(t);
         bf16x8_t pf[4];
         float lt0 = 0.f, lt1 = 0.f;
         nx[0] = nx[1] = f32x16_t{};
@@ -607,23 +615,27 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        }
-        // The barrier orders only this workgroup's LDS use: the compiler may
-        // not move LDS accesses across it, and no wait is needed for the
-        // fragment reads still in flight (their buffer is not written next).
-        wait_lds_dma_but<2 * NI>();
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
+        end_tile();
     };
-    for (int t = 0; t < n; t += 4) {
-        iteration(0, t, xa, xb);
-        if (t + 1 >= n) break;
-        iteration(1, t + 1, xb, xa);
-        if (t + 2 >= n) break;
-        iteration(2, t + 2, xa, xb);
-        if (t + 3 >= n) break;
-        iteration(3, t + 3, xb, xa);
+    if (busy) {
+        for (int t = 0; t < n; t += 4) {
+            iteration(0, t, xa, xb);
+            if (t + 1 >= n) break;
+            iteration(1, t + 1, xb, xa);
+            if (t + 2 >= n) break;
+            iteration(2, t + 2, xa, xb);
+            if (t + 3 >= n) break;
+            iteration(3, t + 3, xb, xa);
+        }
+    } else {
+        // the same loads and barriers, no arithmetic
+        for (int t = 0; t < n; ++t) {
+            refresh(t);
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+                dma_pair(i, kptr, offk[i], kbuf(t), vptr, offv[i], NBUF * TILEB + vbuf(t + 2));
+            end_tile();
+        }
     }
     wait_lds_dma();  // no load may still be writing LDS when the workgroup ends
 
