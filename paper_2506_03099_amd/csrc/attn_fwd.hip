@@ -141,12 +141,23 @@ struct TileRanges {
     int b1, e1;
 };
 
+// Rows [q0, q1) of tile `idx` among the `nt` tiles that cover the rows
+// [begin, end) of one chunk: the chunk's 32-row blocks are split as evenly as
+// possible, so every tile gets the same number of blocks give or take one
+// (at most BM / 32 since nt >= (end - begin) / BM) and tiles take about equally
+// long; only the chunk's last block may be partial.
+template <int BM>
+__device__ __forceinline__ void split_rows(int begin, int end, int nt, int idx, int& q0, int& q1) {
+    const int blocks = (end - begin + 31) / 32;
+    q0 = begin + 32 * ((idx * blocks) / nt);
+    q1 = min(begin + 32 * (((idx + 1) * blocks) / nt), end);
+}
+
 template <int BM>
 __device__ __forceinline__ TileRanges plan_tile(const AttnArgs& a, int tile) {
     TileRanges t;
     if (a.mode == 0) {
-        t.q0 = tile * BM;
-        t.q1 = min(t.q0 + BM, a.Lq);
+        split_rows<BM>(0, a.Lq, a.n_qtiles, tile, t.q0, t.q1);
         t.n = a.n_ranges;
         t.b0 = t.e0 = t.b1 = t.e1 = 0;
         return t;
@@ -157,15 +168,13 @@ __device__ __forceinline__ TileRanges plan_tile(const AttnArgs& a, int tile) {
     int chunk;
     if (nat < a.ref_tiles) {
         chunk = 0;
-        t.q0 = nat * BM;
-        t.q1 = min(t.q0 + BM, a.ref_tok);
+        split_rows<BM>(0, a.ref_tok, a.ref_tiles, nat, t.q0, t.q1);
     } else {
         const int u = nat - a.ref_tiles;
         chunk = 1 + u / a.chunk_tiles;
         const int cs = a.ref_tok + (chunk - 1) * a.chunk_tok;
         const int ce = min(cs + a.chunk_tok, a.seq_len);
-        t.q0 = cs + (u % a.chunk_tiles) * BM;
-        t.q1 = min(t.q0 + BM, ce);
+        split_rows<BM>(cs, ce, (ce - cs + BM - 1) / BM, u % a.chunk_tiles, t.q0, t.q1);
     }
     if (chunk == 0) {
         t.n = 1;
