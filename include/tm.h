@@ -132,6 +132,27 @@ int32_t tm_kv_cache_latest(const tm_kv_cache* cache);
 tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const void* v,
                        int32_t n_tok, hipStream_t stream);
 
+/* Fused K/V producer: RMS normalisation of the chunk's queries and keys, and
+ * the KV append, in one launch. The student keeps the attention of its
+ * WAN2.1 teacher (paper Sec. 4.1), which normalises queries and keys by their
+ * root mean square before the attention equation of Sec. 4.2; the keys cached
+ * for later chunks (Sec. 4.3) are those normalised keys. Each (token, head)
+ * row x of D elements of q and of k becomes
+ *     y[d] = x[d] / sqrt(mean_d(x^2) + eps) * gain[h][d],
+ * computed in fp32 and rounded to the cache dtype (nearest even for bf16).
+ * q, k, v: device [B, n_tok, H, D] in the cache's dtype, as from the QKV
+ * projection. q_out: device, same shape; receives the normalised queries (it
+ * may be q itself, but must not otherwise overlap q, k, v or the pools).
+ * q_gain, k_gain: device fp32 [H, D] (16-byte aligned), or NULL for ones.
+ * eps: finite, >= 0 (TM_E_ARG otherwise). The normalised keys and the values
+ * v go into the cache exactly as tm_kv_append would put k and v (same chunk
+ * order rules, capacities, layouts, zero padding of V and bookkeeping): the
+ * values are copied bit for bit. Replaces a separate normalisation pass and
+ * tm_kv_append. */
+tm_status tm_qkv_produce(tm_kv_cache* cache, int32_t chunk, const void* q, const void* k,
+                         const void* v, const float* q_gain, const float* k_gain, float eps,
+                         void* q_out, int32_t n_tok, hipStream_t stream);
+
 /* Sparse causal attention forward (paper Sec. 4.2, attention equation, over
  * the key set {c_0, c_{a-W}, ..., c_a} of the query's chunk a).
  *

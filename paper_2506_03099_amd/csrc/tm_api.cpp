@@ -314,8 +314,15 @@ tm_status tm_kv_cache_locate(const tm_kv_cache* cache, int32_t chunk, int32_t* t
     return TM_OK;
 }
 
-tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const void* v,
-                       int32_t n_tok, hipStream_t stream) {
+namespace {
+
+// Shared by tm_kv_append and tm_qkv_produce: order and capacity rules, pointer
+// checks, the launch, and the bookkeeping (updated only after a successful
+// launch). With q != nullptr the chunk's queries and keys are RMS-normalised
+// on the way (queries into q_out).
+tm_status write_chunk(tm_kv_cache* cache, int32_t chunk, const void* q, const void* k,
+                      const void* v, const float* q_gain, const float* k_gain, float eps,
+                      void* q_out, int32_t n_tok, hipStream_t stream) {
     if (cache == nullptr) return fail(TM_E_ARG, "cache is NULL");
     Geo g;
     tm_status st = check_desc(&cache->desc, &g);
@@ -336,12 +343,32 @@ tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const v
         return fail(TM_E_ARG, "k/v overlap the cache pools");
     if ((st = check_ptr(cache->k_pool, pool_bytes, "k_pool")) != TM_OK) return st;
     if ((st = check_ptr(cache->v_pool, pool_bytes, "v_pool")) != TM_OK) return st;
+    if (q != nullptr) {
+        if (!std::isfinite(eps) || eps < 0.f) return fail(TM_E_ARG, "eps must be finite and >= 0");
+        if ((st = check_ptr(q, bytes, "q")) != TM_OK) return st;
+        if ((st = check_ptr(q_out, bytes, "q_out")) != TM_OK) return st;
+        if (q_out != q && overlaps(q_out, bytes, q, bytes))
+            return fail(TM_E_ARG, "q_out overlaps q without being q");
+        if (overlaps(q_out, bytes, k, bytes) || overlaps(q_out, bytes, v, bytes) ||
+            overlaps(q_out, bytes, cache->k_pool, pool_bytes) ||
+            overlaps(q_out, bytes, cache->v_pool, pool_bytes))
+            return fail(TM_E_ARG, "q_out overlaps k, v or the cache pools");
+        const size_t gain_bytes = size_t(g.H) * size_t(g.D) * sizeof(float);
+        if (q_gain != nullptr && (st = check_ptr(q_gain, gain_bytes, "q_gain", 16)) != TM_OK) return st;
+        if (k_gain != nullptr && (st = check_ptr(k_gain, gain_bytes, "k_gain", 16)) != TM_OK) return st;
+    }
     const int slot = chunk == 0 ? -1 : int((chunk - 1) % (g.W + 1));
     const int64_t offset = chunk == 0 ? 0 : g.ref_cap + slot * g.slot_cap;
-    const hipError_t e = tmk::launch_kv_append(k, v, cache->k_pool, cache->v_pool, int(g.B), n_tok,
-                                              int(g.H), int(g.D), int(g.elem), g.capacity, offset,
-                                              stream);
-    if (e != hipSuccess) return fail(TM_E_DEVICE, "kv_append launch: %s", hipGetErrorString(e));
+    const hipError_t e =
+        q == nullptr
+            ? tmk::launch_kv_append(k, v, cache->k_pool, cache->v_pool, int(g.B), n_tok, int(g.H),
+                                    int(g.D), int(g.elem), g.capacity, offset, stream)
+            : tmk::launch_qkv_produce(q, k, v, q_out, q_gain, k_gain, eps, cache->k_pool,
+                                      cache->v_pool, int(g.B), n_tok, int(g.H), int(g.D),
+                                      int(g.elem), g.capacity, offset, stream);
+    if (e != hipSuccess)
+        return fail(TM_E_DEVICE, "%s launch: %s", q == nullptr ? "kv_append" : "qkv_produce",
+                    hipGetErrorString(e));
     if (chunk == 0) {
         tm_kv_cache_reset(cache);
         cache->ref_len = n_tok;
@@ -351,6 +378,20 @@ tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const v
     }
     cache->latest = chunk;
     return TM_OK;
+}
+
+}  // namespace
+
+tm_status tm_kv_append(tm_kv_cache* cache, int32_t chunk, const void* k, const void* v,
+                       int32_t n_tok, hipStream_t stream) {
+    return write_chunk(cache, chunk, nullptr, k, v, nullptr, nullptr, 0.f, nullptr, n_tok, stream);
+}
+
+tm_status tm_qkv_produce(tm_kv_cache* cache, int32_t chunk, const void* q, const void* k,
+                         const void* v, const float* q_gain, const float* k_gain, float eps,
+                         void* q_out, int32_t n_tok, hipStream_t stream) {
+    if (q == nullptr) return fail(TM_E_ARG, "q is NULL");
+    return write_chunk(cache, chunk, q, k, v, q_gain, k_gain, eps, q_out, n_tok, stream);
 }
 
 int64_t tm_allowed_pairs(const tm_attn_desc* desc, int32_t q_chunk, const tm_kv_cache* cache,

@@ -68,4 +68,13 @@ hipError_t launch_kv_append(const void* k_src, const void* v_src, void* k_pool, 
                             int B, int n_tok, int H, int D, int elem_bytes, int64_t capacity,
                             int64_t tok_offset, hipStream_t s);
 
+// The same write of the chunk's V, while the chunk's queries (into q_out, same
+// layout as q_src) and keys (into the K pool) are RMS-normalised per (token,
+// head) row over D: x / sqrt(mean(x^2) + eps) * gain[h, :] (gain NULL: ones),
+// in fp32, rounded to the element type. q_out may equal q_src.
+hipError_t launch_qkv_produce(const void* q_src, const void* k_src, const void* v_src, void* q_out,
+                              const float* q_gain, const float* k_gain, float eps, void* k_pool,
+                              void* v_pool, int B, int n_tok, int H, int D, int elem_bytes,
+                              int64_t capacity, int64_t tok_offset, hipStream_t s);
+
 }  // namespace tmk

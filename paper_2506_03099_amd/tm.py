@@ -81,6 +81,8 @@ def lib() -> ctypes.CDLL:
                                                   ctypes.POINTER(ctypes.c_int32)]),
             "tm_kv_cache_latest": (ctypes.c_int32, [P]),
             "tm_kv_append": (ctypes.c_int, [P, ctypes.c_int32, P, P, ctypes.c_int32, P]),
+            "tm_qkv_produce": (ctypes.c_int, [P, ctypes.c_int32, P, P, P, P, P, ctypes.c_float,
+                                              P, ctypes.c_int32, P]),
             "tm_sparse_causal_attn_fwd": (ctypes.c_int, [D, P, ctypes.c_int32, P, P, P,
                                                          ctypes.c_int32, P, P, P]),
             "tm_allowed_pairs": (ctypes.c_int64, [D, ctypes.c_int32, P, ctypes.c_int32]),
@@ -196,6 +198,19 @@ def tm_kv_append(cache: KVCache, chunk: int, k, v, n_tok: int | None = None, str
     if n_tok is None:
         n_tok = k.shape[1]
     _check(lib().tm_kv_append(cache.handle, chunk, _ptr(k), _ptr(v), n_tok, _stream(stream)))
+
+
+def tm_qkv_produce(cache: KVCache, chunk: int, q, k, v, q_gain=None, k_gain=None,
+                   eps: float = 0.0, q_out=None, n_tok: int | None = None, stream=None):
+    """RMS-normalise the chunk's q and k rows and append k (normalised) and v
+    to the cache; returns ``q_out`` (allocated like q if not given)."""
+    if n_tok is None:
+        n_tok = k.shape[1]
+    if q_out is None:
+        q_out = torch.empty_like(q)
+    _check(lib().tm_qkv_produce(cache.handle, chunk, _ptr(q), _ptr(k), _ptr(v), _ptr(q_gain),
+                                _ptr(k_gain), eps, _ptr(q_out), n_tok, _stream(stream)))
+    return q_out
 
 
 def tm_sparse_causal_attn_fwd(desc: tm_attn_desc, q, q_chunk: int, cache: KVCache | None = None,

@@ -109,6 +109,10 @@ def test_append_and_cache_reject_bad_arguments(tm):
     assert L.tm_kv_cache_create(None, FAKE, FAKE, ctypes.byref(h)) == tm.TM_E_ARG
     assert L.tm_kv_cache_reset(None) == tm.TM_E_ARG
     assert L.tm_kv_cache_latest(None) == -1
+    # the fused producer: no cache, or no queries
+    assert L.tm_qkv_produce(None, 0, FAKE, FAKE, FAKE, None, None, 0.0, FAKE, 10, None) == tm.TM_E_ARG
+    assert L.tm_qkv_produce(None, 0, None, FAKE, FAKE, None, None, 0.0, FAKE, 10, None) == tm.TM_E_ARG
+    assert "q is NULL" in tm.tm_last_error()
 
 
 def _oracle_pairs(n_frames, T, C, R, W, q_chunk):
