@@ -23,6 +23,9 @@ What it computes, and where the paper defines it:
   set, used to pin ``attention`` on tiny inputs.
 * ``producer``  -- the RMS normalisation of query and key rows that precedes
   the attention and the KV cache (the fused K/V producer).
+* ``audio``     -- the audio cross-attention of Sec. 4.1: each latent frame's
+  tokens attend to the audio tokens of the five frames centred on it, face
+  tokens only, each face to its own audio stream.
 
 Every function here is pinned by the ``-m "not gpu"`` tests against closed
 forms, invariants, library special cases and the brute force; the one reading
@@ -43,3 +46,4 @@ from .attention import (  # noqa: F401
 )
 from .brute import brute_force_attention  # noqa: F401
 from .producer import rms_normalise  # noqa: F401
+from .audio import audio_cross_attention, audio_window  # noqa: F401
