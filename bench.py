@@ -239,6 +239,9 @@ def main():
     del cache, dev, chunks
     torch.cuda.empty_cache()
 
+    # ---------------------------------------------------------------- audio cross-attention
+    result["audio_cross_attn"] = audio_cross_attn(torch, tm, stream, args.steps)
+
     # ---------------------------------------------------------------- other workloads
     if args.other_workloads:
         result["other_workloads"] = other_workloads(torch, tm, WORKLOADS, stream)
@@ -253,6 +256,54 @@ def main():
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def audio_cross_attn(torch, tm, stream, steps):
+    """The audio cross-attention of the 480p chunk (frames 4..6 of 21, one
+    face of 14% of the tokens, 32 audio tokens per latent frame, five-frame
+    window), launched back to back. HBM-bound: algorithmic bytes are every
+    output row written, the queries of face rows read, the face ids and the
+    audio keys and values of the chunk's windows read once."""
+    from synth import AUDIO_WORKLOADS, draw_audio
+    w = AUDIO_WORKLOADS["wan14b_480p_audio_chunk"]
+    d = draw_audio(w)
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, ak, av = dev(d["q_bits"]), dev(d["ak_bits"]), dev(d["av_bits"])
+    face = torch.from_numpy(d["face"]).cuda()
+    o = torch.empty_like(q)
+    desc = tm.make_audio_desc(w.batch, w.heads, w.head_dim, w.tokens_per_frame, w.audio_per_frame,
+                              w.audio_frames, w.streams, w.half_window)
+    call = lambda: tm.tm_audio_cross_attn_fwd(desc, q, w.first_frame, ak, av, face, o=o)
+    for _ in range(20):
+        call()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        call()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    row = w.heads * w.head_dim * 2
+    face_rows = int((d["face"] >= 0).sum())
+    lo = max(0, w.first_frame - w.half_window)
+    hi = min(w.audio_frames - 1, w.first_frame + w.n_frames - 1 + w.half_window)
+    audio_tok = (hi - lo + 1) * w.audio_per_frame * w.streams * w.batch
+    nbytes = w.batch * w.n_tok * row + face_rows * row + d["face"].nbytes + 2 * audio_tok * row
+    keys = [(min(w.audio_frames - 1, f + w.half_window) - max(0, f - w.half_window) + 1)
+            * w.audio_per_frame for f in range(w.first_frame, w.first_frame + w.n_frames)]
+    per_frame = d["face"][0].reshape(w.n_frames, -1) >= 0
+    flop = sum(4.0 * w.head_dim * w.heads * int(per_frame[i].sum()) * keys[i]
+               for i in range(w.n_frames)) * w.batch
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    return {"workload": w.name, "kernel": "audio_attn_bf16_kernel<128>", "bound": "hbm",
+            "us": round(ms * 1e3, 2), "algorithmic_mb": round(nbytes / 1e6, 2),
+            "gbps": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM_GBPS, 4),
+            "face_fraction": round(face_rows / (w.batch * w.n_tok), 4),
+            "keys_per_face_row": keys, "tflops": round(flop / (ms * 1e-3) / 1e12, 2)}
 
 
 def timing_inputs(torch, shape, seed):

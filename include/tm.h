@@ -184,6 +184,46 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
 int64_t tm_allowed_pairs(const tm_attn_desc* desc, int32_t q_chunk, const tm_kv_cache* cache,
                          int32_t n_frames);
 
+/* Audio cross-attention with a local frame window and a face mask (paper
+ * Sec. 4.1: "Audio Cross Attention with Attention Mask", "Audio Projection
+ * Layer", "Speaking/Silence Mode"). Audio tokens are aligned to latent frames,
+ * A per frame, covering frames 0 .. F_a - 1; each face has its own audio
+ * stream (a silent face's stream holds the special embedding's keys and
+ * values). A query token of latent frame f whose face id is m in [0, M)
+ * attends, with exact softmax(q k^T * scale) v, to the audio tokens of stream
+ * m in frames max(0, f - w) .. min(F_a - 1, f + w) (w = 2: five frames centred
+ * on f); a token with any other face id (-1: no face) gets a zero output. */
+#define TM_MAX_AUDIO_STREAMS 32
+
+typedef struct tm_audio_desc {
+    int32_t batch;            /* B >= 1 */
+    int32_t heads;            /* H >= 1 */
+    int32_t head_dim;         /* D: 64 or 128 */
+    int32_t tokens_per_frame; /* T >= 1: query tokens per latent frame */
+    int32_t audio_per_frame;  /* A >= 1: audio tokens per latent frame */
+    int32_t audio_frames;     /* F_a >= 1: latent frames the audio covers */
+    int32_t streams;          /* M in [1, TM_MAX_AUDIO_STREAMS]: audio streams (faces) */
+    int32_t half_window;      /* w >= 0 (paper: 2, a window of five frames) */
+    int32_t dtype;            /* TM_BF16 only; accumulation is fp32 */
+    float softmax_scale;      /* > 0, or <= 0 for 1/sqrt(D) */
+} tm_audio_desc;
+
+/* q: device [B, n_tok, H, D], query row i in latent frame
+ * first_frame + i / T; every frame of the run must lie inside the audio
+ * (first_frame + ceil(n_tok / T) <= F_a, else TM_E_SHAPE).
+ * ak, av: device [B, M, F_a * A, H, D] audio keys and values.
+ * face: device int32 [B, n_tok] (4-byte aligned), the stream of each query
+ * token; ids outside [0, M) mean no face.
+ * o: device [B, n_tok, H, D], every row written; may be q itself (in place)
+ * but must not otherwise overlap q, ak, av or face.
+ * A frame's window (at most (2w + 1) * A keys, rounded up to 32) must fit in
+ * one workgroup's LDS: at most 288 keys at D = 128, 608 at D = 64, else
+ * TM_E_SHAPE. n_tok = 0 launches nothing. P is rounded to bf16 before P V and
+ * the row sums use the rounded P; the result is deterministic. */
+tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* desc, const void* q, int32_t first_frame,
+                                  int32_t n_tok, const void* ak, const void* av,
+                                  const int32_t* face, void* o, hipStream_t stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* tm_last_error(void);
 

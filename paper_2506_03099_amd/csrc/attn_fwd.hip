@@ -38,20 +38,16 @@
 #include <math.h>
 #include <stdint.h>
 
+#include "tm_device.h"
 #include "tm_internal.h"
 
 namespace tmk {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
-constexpr float kNegInf = -__builtin_inff();
 // Threads per workgroup of the bf16 kernel: 8 waves (two per SIMD) sharing
 // every K/V tile staged in LDS.
 constexpr int kBf16Threads = 512;
@@ -120,16 +116,6 @@ __device__ __forceinline__ void wait_lds_dma_but() {
 __device__ __forceinline__ float pin(float x) {
     asm volatile("" : "+v"(x));
     return x;
-}
-
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
-// Renumber them so that consecutive logical ids (the query tiles of one head,
-// which stream the same K/V) land on the same XCD.
-__device__ __forceinline__ int xcd_logical_id(int bid, int total) {
-    constexpr int kXcds = 8;
-    const int per = total / kXcds, rem = total % kXcds;
-    const int x = bid % kXcds, j = bid / kXcds;
-    return x * per + min(x, rem) + j;
 }
 
 // Query rows [q0, q1) of tile `tile` and its key ranges. Mode 0 reads the
@@ -221,17 +207,7 @@ __device__ __forceinline__ f32x16_t mfma32x32x16(bf16x8_t a, bf16x8_t b, f32x16_
 // consecutive rows) over distinct banks. Tiles are filled by direct
 // global->LDS loads (global_load_lds_dwordx4): each wave instruction writes
 // 1 KB of LDS linearly, so each lane fetches the global chunk that belongs at
-// its LDS position.
-template <int D>
-__device__ __forceinline__ int lds_swizzle(int row) {
-    // Low three bits: a permutation of 0..7 over any 8 aligned rows (K reads
-    // of one chunk from 8 consecutive rows hit 8 distinct 16-byte bank
-    // groups), with bits 1-2 distinct over any 4 aligned rows (the V reads'
-    // chunk pairs {p, p^1} of 4 consecutive rows are disjoint). Bit 3 (rows
-    // of 16 chunks only) separates rows r and r + 8.
-    const int low = 2 * (row & 3) + ((row >> 2) & 1);
-    return D == 128 ? low + 8 * ((row >> 3) & 1) : low;
-}
+// its LDS position (lds_swizzle).
 
 // V^T tile: D rows of 64 keys (128 bytes, 8 chunks of 8 keys). Chunk c of row
 // d sits at position c ^ vt_swizzle(d): over any 16 consecutive rows the pair
@@ -239,11 +215,6 @@ __device__ __forceinline__ int lds_swizzle(int row) {
 // chunk of 16 consecutive rows hit 64 distinct banks.
 __device__ __forceinline__ int vt_swizzle(int d) { return (d >> 1) & 7; }
 
-// Row of the K tile that feeds S^T row r when V is read as V^T: bits 2 and 3
-// of r swapped. The S^T output register i of a lane in half-wave hw then holds
-// key 16*(i/8) + 8*hw + i%8 of its 32-key block, so the 8 P^T elements a lane
-// feeds to a 16-key MFMA step are 8 consecutive keys.
-__device__ __forceinline__ int k_perm(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
 
 

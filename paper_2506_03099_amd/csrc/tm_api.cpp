@@ -492,6 +492,90 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
     return TM_OK;
 }
 
+tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t first_frame,
+                                  int32_t n_tok, const void* ak, const void* av,
+                                  const int32_t* face, void* o, hipStream_t stream) {
+    if (d == nullptr) return fail(TM_E_ARG, "descriptor is NULL");
+    if (d->dtype != TM_BF16) return fail(TM_E_DTYPE, "audio cross-attention runs in TM_BF16 only");
+    if (d->batch < 1 || d->heads < 1) return fail(TM_E_SHAPE, "batch and heads must be >= 1");
+    if (int64_t(d->batch) * d->heads > (int64_t(1) << 20))
+        return fail(TM_E_SHAPE, "batch * heads too large");
+    if (d->head_dim != 64 && d->head_dim != 128)
+        return fail(TM_E_SHAPE, "head_dim %d unsupported (64 or 128)", d->head_dim);
+    if (d->tokens_per_frame < 1 || d->audio_per_frame < 1 || d->audio_frames < 1)
+        return fail(TM_E_SHAPE, "tokens_per_frame, audio_per_frame and audio_frames must be >= 1");
+    if (d->streams < 1 || d->streams > TM_MAX_AUDIO_STREAMS)
+        return fail(TM_E_SHAPE, "streams %d outside [1, %d]", d->streams, TM_MAX_AUDIO_STREAMS);
+    if (d->half_window < 0) return fail(TM_E_SHAPE, "half_window must be >= 0");
+    if (!std::isfinite(d->softmax_scale)) return fail(TM_E_ARG, "softmax_scale is not finite");
+    const int64_t La = int64_t(d->audio_frames) * d->audio_per_frame;
+    if (La > kMaxTokens) return fail(TM_E_SHAPE, "audio too long (more than 2^30 tokens)");
+    if (n_tok < 0 || first_frame < 0) return fail(TM_E_SHAPE, "n_tok and first_frame must be >= 0");
+    if (n_tok == 0) return TM_OK;  // nothing to attend
+    const int64_t T = d->tokens_per_frame;
+    const int64_t n_frames = ceil_div(n_tok, T);
+    if (int64_t(first_frame) + n_frames > d->audio_frames)
+        return fail(TM_E_SHAPE, "query frames %d..%lld lie past the audio's %d frames", first_frame,
+                    static_cast<long long>(first_frame + n_frames - 1), d->audio_frames);
+    // The widest window of the run's frames must fit the workgroup's LDS.
+    int64_t max_keys = 0;
+    for (int64_t f = first_frame; f < first_frame + n_frames; ++f) {
+        const int64_t lo = std::max<int64_t>(0, f - d->half_window);
+        const int64_t hi = std::min<int64_t>(d->audio_frames - 1, f + d->half_window);
+        max_keys = std::max(max_keys, (hi - lo + 1) * d->audio_per_frame);
+    }
+    if (max_keys > kMaxTokens) return fail(TM_E_SHAPE, "audio window too long");
+    const int64_t keys_pad = round_up(max_keys, 32);
+    if (tmk::audio_lds_bytes(d->head_dim, int(keys_pad)) > tmk::kAudioMaxLds)
+        return fail(TM_E_SHAPE, "audio window of %lld keys does not fit in LDS (at most %d keys at D = %d)",
+                    static_cast<long long>(max_keys), d->head_dim == 128 ? 288 : 608, d->head_dim);
+
+    const size_t HD = size_t(d->heads) * size_t(d->head_dim);
+    const size_t q_bytes = size_t(d->batch) * size_t(n_tok) * HD * 2;
+    const size_t a_bytes = size_t(d->batch) * size_t(d->streams) * size_t(La) * HD * 2;
+    const size_t f_bytes = size_t(d->batch) * size_t(n_tok) * sizeof(int32_t);
+    tm_status st;
+    if ((st = check_ptr(q, q_bytes, "q")) != TM_OK) return st;
+    if ((st = check_ptr(ak, a_bytes, "ak")) != TM_OK) return st;
+    if ((st = check_ptr(av, a_bytes, "av")) != TM_OK) return st;
+    if ((st = check_ptr(face, f_bytes, "face", 4)) != TM_OK) return st;
+    if ((st = check_ptr(o, q_bytes, "o")) != TM_OK) return st;
+    if (overlaps(o, q_bytes, ak, a_bytes) || overlaps(o, q_bytes, av, a_bytes) ||
+        overlaps(o, q_bytes, face, f_bytes))
+        return fail(TM_E_ARG, "o overlaps ak, av or face");
+    if (o != q && overlaps(o, q_bytes, q, q_bytes))
+        return fail(TM_E_ARG, "o partially overlaps q (only o == q is allowed)");
+
+    const int64_t rows_per_frame = std::min<int64_t>(T, n_tok);
+    const int64_t blocks = ceil_div(rows_per_frame, 32);
+    const int64_t parts = ceil_div(blocks, tmk::kAudioBlocksPerPart);
+    if (int64_t(d->batch) * d->heads * n_frames * parts > INT32_MAX)
+        return fail(TM_E_SHAPE, "grid too large");
+    tmk::AudioArgs a{};
+    a.q = q;
+    a.ak = ak;
+    a.av = av;
+    a.face = face;
+    a.o = o;
+    a.B = d->batch;
+    a.n = n_tok;
+    a.H = d->heads;
+    a.M = d->streams;
+    a.La = int32_t(La);
+    a.T = d->tokens_per_frame;
+    a.A = d->audio_per_frame;
+    a.first_frame = first_frame;
+    a.half_window = d->half_window;
+    a.n_frames = int32_t(n_frames);
+    a.parts = int32_t(parts);
+    a.max_keys_pad = int32_t(keys_pad);
+    const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt(float(d->head_dim));
+    a.scale_log2 = float(double(scale) * 1.4426950408889634);
+    const hipError_t e = tmk::launch_audio_attn_bf16(a, d->head_dim, stream);
+    if (e != hipSuccess) return fail(TM_E_DEVICE, "audio attention launch: %s", hipGetErrorString(e));
+    return TM_OK;
+}
+
 const char* tm_last_error(void) { return g_err.c_str(); }
 
 }  // extern "C"

@@ -1,5 +1,6 @@
 // Internal interface between the host-side API (tm_api.cpp) and the HIP
-// kernels (attn_fwd.hip, kv_append.hip). Not part of the public ABI.
+// kernels (attn_fwd.hip, kv_append.hip, audio_attn.hip). Not part of the
+// public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -76,5 +77,43 @@ hipError_t launch_qkv_produce(const void* q_src, const void* k_src, const void* 
                               const float* q_gain, const float* k_gain, float eps, void* k_pool,
                               void* v_pool, int B, int n_tok, int H, int D, int elem_bytes,
                               int64_t capacity, int64_t tok_offset, hipStream_t s);
+
+// Audio cross-attention of a run of latent-frame tokens (bf16). q, o: [B, n,
+// H, D]; ak, av: [B, M, La, H, D] with La = F_a * A; face: [B, n] stream index
+// per query token (ids outside [0, M) mean no face: zero output).
+struct AudioArgs {
+    const void* q;
+    const void* ak;
+    const void* av;
+    const int32_t* face;
+    void* o;
+    int32_t B, n, H, M, La;
+    int32_t T;             // query tokens per latent frame
+    int32_t A;             // audio tokens per latent frame
+    int32_t first_frame;   // latent frame of query row 0
+    int32_t half_window;   // frames f - w .. f + w
+    int32_t n_frames;      // latent frames the n rows span
+    int32_t parts;         // workgroups per (batch, head, frame)
+    int32_t max_keys_pad;  // most window keys of any frame, rounded up to 32
+    float scale_log2;      // softmax scale * log2(e)
+};
+
+// Most 32-row blocks of one frame per audio workgroup: a frame with more
+// blocks is split over several workgroups, which take every parts-th block.
+constexpr int kAudioBlocksPerPart = 32;
+
+// LDS of one audio workgroup: a window of nk_pad keys as K rows and V rows of
+// D bf16 each, then the face ids of the workgroup's rows and one word per
+// wave.
+constexpr size_t kAudioFaceLds = 4 * 32 * kAudioBlocksPerPart + 4 * 8;
+__host__ __device__ constexpr size_t audio_lds_bytes(int head_dim, int nk_pad) {
+    return 2 * static_cast<size_t>(nk_pad) * head_dim * 2 + kAudioFaceLds;
+}
+constexpr size_t kAudioMaxLds = 160 * 1024;  // gfx950: 160 KiB of LDS per workgroup
+// Most window keys (a multiple of 32) that fit: 288 at D = 128, 608 at D = 64.
+template <int D>
+constexpr int kAudioMaxKeys = static_cast<int>((kAudioMaxLds - kAudioFaceLds) / (2 * 2 * D)) / 32 * 32;
+
+hipError_t launch_audio_attn_bf16(const AudioArgs& a, int head_dim, hipStream_t s);
 
 }  // namespace tmk

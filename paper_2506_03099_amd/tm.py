@@ -26,6 +26,7 @@ TM_E_DEVICE = -6
 TM_F32 = 0
 TM_BF16 = 1
 TM_MAX_WINDOW = 12
+TM_MAX_AUDIO_STREAMS = 32
 
 STATUS_NAMES = {0: "TM_OK", -1: "TM_E_ARG", -2: "TM_E_SHAPE", -3: "TM_E_DTYPE",
                 -4: "TM_E_ORDER", -5: "TM_E_CAPACITY", -6: "TM_E_DEVICE"}
@@ -51,6 +52,21 @@ class tm_attn_desc(ctypes.Structure):
         return _TORCH_DTYPE[self.dtype]
 
 
+class tm_audio_desc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("tokens_per_frame", ctypes.c_int32),
+        ("audio_per_frame", ctypes.c_int32),
+        ("audio_frames", ctypes.c_int32),
+        ("streams", ctypes.c_int32),
+        ("half_window", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+    ]
+
+
 class TMError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
@@ -70,6 +86,7 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(_LIB_PATH)
         P = ctypes.c_void_p
         D = ctypes.POINTER(tm_attn_desc)
+        AD = ctypes.POINTER(tm_audio_desc)
         sig = {
             "tm_kv_cache_tokens": (ctypes.c_int64, [D]),
             "tm_kv_cache_bytes": (ctypes.c_size_t, [D]),
@@ -86,6 +103,8 @@ def lib() -> ctypes.CDLL:
             "tm_sparse_causal_attn_fwd": (ctypes.c_int, [D, P, ctypes.c_int32, P, P, P,
                                                          ctypes.c_int32, P, P, P]),
             "tm_allowed_pairs": (ctypes.c_int64, [D, ctypes.c_int32, P, ctypes.c_int32]),
+            "tm_audio_cross_attn_fwd": (ctypes.c_int, [AD, P, ctypes.c_int32, ctypes.c_int32, P, P,
+                                                       P, P, P]),
             "tm_last_error": (ctypes.c_char_p, []),
         }
         for name, (res, args) in sig.items():
@@ -223,4 +242,29 @@ def tm_sparse_causal_attn_fwd(desc: tm_attn_desc, q, q_chunk: int, cache: KVCach
     _check(lib().tm_sparse_causal_attn_fwd(ctypes.byref(desc), _ptr(q), q_chunk, h, _ptr(k),
                                            _ptr(v), n_frames, _ptr(o), _ptr(lse),
                                            _stream(stream)))
+    return o
+
+
+def make_audio_desc(batch, heads, head_dim, tokens_per_frame, audio_per_frame, audio_frames,
+                    streams=1, half_window=2, dtype="bf16", softmax_scale=0.0) -> tm_audio_desc:
+    if isinstance(dtype, torch.dtype):
+        dtype = {torch.float32: TM_F32, torch.bfloat16: TM_BF16}[dtype]
+    elif isinstance(dtype, str):
+        dtype = {"f32": TM_F32, "bf16": TM_BF16}[dtype]
+    return tm_audio_desc(batch, heads, head_dim, tokens_per_frame, audio_per_frame, audio_frames,
+                         streams, half_window, dtype, softmax_scale)
+
+
+def tm_audio_cross_attn_fwd(desc: tm_audio_desc, q, first_frame: int, ak, av, face, o=None,
+                            n_tok: int | None = None, stream=None):
+    """Audio cross-attention of the query rows ``q`` ([B, n_tok, H, D], row i
+    in latent frame first_frame + i // T) over the audio keys/values ``ak``,
+    ``av`` ([B, M, F_a * A, H, D]) with int32 face ids ``face`` ([B, n_tok]);
+    returns ``o`` (allocated like q if not given)."""
+    if n_tok is None:
+        n_tok = q.shape[1]
+    if o is None:
+        o = torch.empty_like(q)
+    _check(lib().tm_audio_cross_attn_fwd(ctypes.byref(desc), _ptr(q), first_frame, n_tok, _ptr(ak),
+                                         _ptr(av), _ptr(face), _ptr(o), _stream(stream)))
     return o

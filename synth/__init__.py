@@ -12,4 +12,8 @@ from .inputs import (  # noqa: F401
     draw_tensor,
     draw_qkv_sequence,
     draw_chunk,
+    AudioWorkload,
+    AUDIO_WORKLOADS,
+    face_ids,
+    draw_audio,
 )

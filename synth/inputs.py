@@ -181,3 +181,92 @@ def draw_qkv_sequence(w: Workload, n_frames: int | None = None, *, step: int = 0
         if w.dtype == "bf16":
             res[name + "_bits"] = np.stack([pb[i][1] for pb in per_b])
     return res
+
+
+# --------------------------------------------------------------------------- audio cross-attention
+
+
+@dataclass(frozen=True)
+class AudioWorkload:
+    """Shape of one synthetic audio cross-attention workload.
+
+    The query rows are ``n_frames`` latent frames of a ``grid_h x grid_w``
+    patch grid starting at latent frame ``first_frame``; the audio holds
+    ``audio_per_frame`` tokens per latent frame for ``audio_frames`` frames and
+    ``streams`` faces; ``half_window`` frames on each side (2: five frames).
+    """
+
+    wid: int
+    name: str
+    batch: int
+    heads: int
+    head_dim: int
+    grid_h: int
+    grid_w: int
+    audio_per_frame: int
+    audio_frames: int
+    streams: int
+    half_window: int
+    first_frame: int
+    n_frames: int
+    notes: str = field(default="", compare=False)
+
+    @property
+    def tokens_per_frame(self) -> int:
+        return self.grid_h * self.grid_w
+
+    @property
+    def n_tok(self) -> int:
+        return self.n_frames * self.tokens_per_frame
+
+
+AUDIO_WORKLOADS: dict[str, AudioWorkload] = {
+    w.name: w
+    for w in [
+        AudioWorkload(20, "wan14b_480p_audio_chunk", 1, 40, 128, 30, 52, 32, 21, 1, 2, 4, 3,
+                      notes="one 3-frame chunk (frames 4..6 of 21) of 1560 tokens per frame, "
+                            "one face, 32 audio tokens per latent frame, five-frame window"),
+        AudioWorkload(21, "wan14b_480p_audio_2faces", 1, 8, 128, 30, 52, 32, 21, 2, 2, 18, 3,
+                      notes="the last chunk (frames 18..20, windows clipped), two faces"),
+    ]
+}
+
+
+def face_ids(grid_h: int, grid_w: int, n_frames: int, streams: int, batch: int = 1):
+    """Face id of every token, int32 ``[batch, n_frames * grid_h * grid_w]``:
+    ``streams`` elliptical face regions side by side in the upper half of
+    every frame (face m centred at column (m + 1) / (streams + 1) of the
+    width, row 0.4 of the height; semi-axes 0.4 / (streams + 1) of the width
+    and 0.22 of the height), -1 elsewhere."""
+    y, x = np.meshgrid(np.arange(grid_h) + 0.5, np.arange(grid_w) + 0.5, indexing="ij")
+    ids = np.full((grid_h, grid_w), -1, dtype=np.int32)
+    ry = 0.22 * grid_h
+    rx = 0.4 * grid_w / (streams + 1)
+    for m in range(streams):
+        cx = grid_w * (m + 1) / (streams + 1)
+        cy = 0.4 * grid_h
+        ids[((x - cx) / rx) ** 2 + ((y - cy) / ry) ** 2 <= 1.0] = m
+    frame = ids.reshape(-1)
+    return np.broadcast_to(np.tile(frame, n_frames), (batch, n_frames * frame.size)).copy()
+
+
+def draw_audio(w: AudioWorkload, *, layer: int = 0, base_seed: int = 0):
+    """Seeded bf16 inputs of an audio workload.
+
+    q ``[B, n_tok, H, D]`` and the audio keys ``ak`` ``[B, M, F_a * A, H, D]``
+    are RMS-normalised per (token, head) row, the audio values ``av`` are
+    N(0, 1); all rounded to bfloat16. Returns a dict with the fp32 values
+    (``q, ak, av``), their bit patterns (``*_bits``) and ``face`` (int32).
+    """
+    La = w.audio_frames * w.audio_per_frame
+    res = {}
+    for name, shape, tid, norm in (
+            ("q", (w.batch, w.n_tok, w.heads, w.head_dim), TENSOR_Q, True),
+            ("ak", (w.batch, w.streams, La, w.heads, w.head_dim), TENSOR_K, True),
+            ("av", (w.batch, w.streams, La, w.heads, w.head_dim), TENSOR_V, False)):
+        vals, bits = draw_tensor(shape, wid=w.wid, b=0, chunk=w.first_frame, step=0, layer=layer,
+                                 tensor_id=tid, rms_normalise=norm, dtype="bf16",
+                                 base_seed=base_seed)
+        res[name], res[name + "_bits"] = vals, bits
+    res["face"] = face_ids(w.grid_h, w.grid_w, w.n_frames, w.streams, w.batch)
+    return res

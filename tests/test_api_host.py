@@ -147,3 +147,52 @@ def test_planner_pair_counts_equal_oracle_mask_counts(tm, n_frames, T, C, R, W):
 def test_planner_full_sequence_480p_total(tm):
     d = _desc(tm)
     assert tm.tm_allowed_pairs(d, -1, None, 21) == 316_368_000
+
+
+# --------------------------------------------------------------------------- audio cross-attention
+
+
+def _adesc(tm, **kw):
+    base = dict(batch=1, heads=40, head_dim=128, tokens_per_frame=1560, audio_per_frame=32,
+                audio_frames=21, streams=1, half_window=2, dtype=tm.TM_BF16, softmax_scale=0.0)
+    base.update(kw)
+    return tm.tm_audio_desc(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=0), -3), (dict(dtype=9), -3), (dict(head_dim=96), -2), (dict(batch=0), -2),
+    (dict(heads=0), -2), (dict(tokens_per_frame=0), -2), (dict(audio_per_frame=0), -2),
+    (dict(audio_frames=0), -2), (dict(streams=0), -2), (dict(streams=33), -2),
+    (dict(half_window=-1), -2), (dict(softmax_scale=float("nan")), -1),
+    # windows that do not fit one workgroup's LDS: 5 * 58 = 290 > 288 keys at D = 128
+    (dict(audio_per_frame=58), -2), (dict(head_dim=64, audio_per_frame=122), -2),
+])
+def test_audio_rejects_bad_descriptor(tm, kw, status):
+    d = _adesc(tm, **kw)
+    st = tm.lib().tm_audio_cross_attn_fwd(ctypes.byref(d), FAKE, 0, 4680, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == status, tm.tm_last_error()
+    assert tm.tm_last_error() != ""
+
+
+def test_audio_rejects_bad_arguments(tm):
+    L = tm.lib()
+    d = _adesc(tm)
+    call = lambda ff, n, q=FAKE, ak=FAKE, av=FAKE, face=FAKE, o=FAKE: L.tm_audio_cross_attn_fwd(
+        ctypes.byref(d), q, ff, n, ak, av, face, o, None)
+    assert L.tm_audio_cross_attn_fwd(None, FAKE, 0, 10, FAKE, FAKE, FAKE, FAKE, None) == tm.TM_E_ARG
+    assert call(0, 0) == tm.TM_OK                    # nothing to attend: no launch, no checks
+    assert call(-1, 10) == tm.TM_E_SHAPE
+    assert call(0, -1) == tm.TM_E_SHAPE
+    assert call(19, 3 * 1560) == tm.TM_E_SHAPE       # frames 19..21, audio covers 0..20
+    assert call(18, 3 * 1560 + 1) == tm.TM_E_SHAPE   # a 4th, partial frame: 18..21
+    assert call(18, 3 * 1560, q=None) == tm.TM_E_ARG
+    assert call(18, 3 * 1560, face=FAKE + 2) == tm.TM_E_ARG   # misaligned
+    assert call(18, 3 * 1560) == tm.TM_E_ARG          # not device memory
+    # the widest window fits: 288 keys at D = 128 (A = 57, w = 2: 285 keys)
+    ok = _adesc(tm, audio_per_frame=57)
+    st = L.tm_audio_cross_attn_fwd(ctypes.byref(ok), FAKE, 0, 10, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == tm.TM_E_ARG  # passes the shape checks, fails on the fake pointers
+    # near the ends of the audio the window is clipped, so a wider A can fit there
+    edge = _adesc(tm, audio_per_frame=90, audio_frames=3)  # frames 0..2: at most 3 * 90 = 270 keys
+    st = L.tm_audio_cross_attn_fwd(ctypes.byref(edge), FAKE, 0, 1560, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == tm.TM_E_ARG

@@ -1,0 +1,193 @@
+"""GPU parity of the audio cross-attention (tm_audio_cross_attn_fwd) against
+the oracle (``oracle.audio_cross_attention``, fp32 on the same bf16 values).
+
+Face rows are compared element by element to the bf16 bar with the output
+rounding term: |err| <= 2e-2 x RMS(compared rows) + 2^-8 |o_oracle|. A window
+holds at most a few hundred keys (160 in the paper's setting), so |o| has a
+heavy tail (up to several times its RMS) and rounding the exact output to
+bf16 alone costs up to 2^-8 |o|, as for the attention's small geometries;
+rows without a face, and rows whose face id is outside [0, M), must be exactly
+zero. Cases: ragged row blocks and a partial last frame, windows clipped at
+both ends of the audio, a window padded to the next 32 keys, several streams
+mixed inside one 32-row block, frames split over several workgroups, the
+largest window that fits in LDS, in-place output, no rows, and the 480p
+workloads (two faces in full, one face on sampled heads and rows).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import assert_close, say
+from oracle import audio_cross_attention
+from synth import AUDIO_WORKLOADS, bf16_bits_to_f32, draw_audio, f32_to_bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tm():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2506_03099_amd import tm as binding
+    binding.lib()
+    return binding
+
+
+def _bf16(rng, shape, norm):
+    x = rng.standard_normal(shape).astype(np.float32)
+    if norm:
+        x /= np.sqrt(np.mean(x * x, axis=-1, keepdims=True))
+    bits = f32_to_bf16_bits(x)
+    return bf16_bits_to_f32(bits), bits
+
+
+def _dev(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _inputs(seed, B, n, H, D, M, La):
+    rng = np.random.default_rng(seed)
+    q, qb = _bf16(rng, (B, n, H, D), True)
+    ak, akb = _bf16(rng, (B, M, La, H, D), True)
+    av, avb = _bf16(rng, (B, M, La, H, D), False)
+    return rng, (q, ak, av), (_dev(qb), _dev(akb), _dev(avb))
+
+
+def _check(o_dev, q, ak, av, face, T, A, first, w, what, heads=None, rows=None):
+    M = ak.shape[1]
+    valid = np.where((face >= 0) & (face < M), face, -1)  # other ids mean no face
+    o = o_dev.float().cpu().numpy()
+    if heads is not None:
+        o = o[:, :, heads]
+    if rows is not None:
+        o = o[:, rows]
+        valid_r = valid[:, rows]
+    else:
+        valid_r = valid
+    want = audio_cross_attention(q, ak, av, valid, tokens_per_frame=T, audio_per_frame=A,
+                                 first_frame=first, half_window=w, heads=heads, rows=rows)
+    sel = valid_r >= 0
+    assert np.all(o[~sel] == 0), f"{what}: rows without a face are not zero"
+    assert sel.any()
+    assert_close(o[sel], want[sel], "bf16", what, output_rounding=True)
+
+
+@pytest.mark.parametrize("D", [128, 64])
+@pytest.mark.parametrize("first", [0, 2, 6])
+def test_audio_matches_oracle_small(tm, D, first):
+    B, H, T, A, Fa, M, w, frames = 2, 3, 50, 7, 9, 3, 2, 3
+    say(f"audio vs oracle: D={D} first_frame={first}")
+    n = T * frames
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(100 + D + first, B, n, H, D, M, Fa * A)
+    face = rng.choice([-1, 0, 1, 2, 3, 7, -5], size=(B, n),
+                      p=[0.25, 0.2, 0.2, 0.2, 0.05, 0.05, 0.05]).astype(np.int32)
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = tm.tm_audio_cross_attn_fwd(desc, qd, first, akd, avd, torch.from_numpy(face).cuda())
+    torch.cuda.synchronize()
+    _check(o, q, ak, av, face, T, A, first, w, f"D={D} first={first}")
+
+
+@pytest.mark.parametrize("T,A,n_extra", [(70, 32, 35), (1100, 33, 100), (2100, 32, 0)])
+def test_audio_ragged_rows_split_frames_and_padded_windows(tm, T, A, n_extra):
+    # T = 70: blocks of 32, 32, 6 rows; T = 1100: 35 blocks, two workgroups per
+    # frame taking every other block; T = 2100: 66 blocks, three workgroups;
+    # A = 33: 165 keys padded to 192; a partial last frame
+    B, H, D, Fa, M, w, first = 1, 2, 128, 6, 2, 2, 1
+    n = 2 * T + n_extra
+    say(f"audio ragged: T={T} A={A} n={n}")
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(T + A, B, n, H, D, M, Fa * A)
+    face = rng.choice([-1, 0, 1], size=(B, n)).astype(np.int32)
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = tm.tm_audio_cross_attn_fwd(desc, qd, first, akd, avd, torch.from_numpy(face).cuda())
+    torch.cuda.synchronize()
+    _check(o, q, ak, av, face, T, A, first, w, f"T={T} A={A}")
+
+
+@pytest.mark.parametrize("w,Fa,A", [(0, 5, 16), (1, 5, 16), (10, 4, 16)])
+def test_audio_window_extremes(tm, w, Fa, A):
+    # w = 0: a frame's own audio only; w = 10 over 4 frames: all audio
+    B, H, D, T, M = 1, 2, 128, 40, 1
+    frames = min(Fa, 3)
+    n = T * frames
+    say(f"audio window w={w} Fa={Fa}")
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(7 + w, B, n, H, D, M, Fa * A)
+    face = np.where(rng.random((B, n)) < 0.7, 0, -1).astype(np.int32)
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = tm.tm_audio_cross_attn_fwd(desc, qd, 0, akd, avd, torch.from_numpy(face).cuda())
+    torch.cuda.synchronize()
+    _check(o, q, ak, av, face, T, A, 0, w, f"w={w}")
+
+
+@pytest.mark.parametrize("D,A", [(128, 57), (64, 121)])
+def test_audio_largest_window_that_fits(tm, D, A):
+    # (2w + 1) * A = 285 keys padded to 288 at D = 128, 605 padded to 608 at
+    # D = 64: the LDS limit
+    B, H, T, Fa, M, w = 1, 2, 64, 5, 1, 2
+    n = T
+    say(f"audio largest window: D={D} A={A}")
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(D + A, B, n, H, D, M, Fa * A)
+    face = np.zeros((B, n), dtype=np.int32)
+    face[:, ::5] = -1
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = tm.tm_audio_cross_attn_fwd(desc, qd, 2, akd, avd, torch.from_numpy(face).cuda())
+    torch.cuda.synchronize()
+    _check(o, q, ak, av, face, T, A, 2, w, f"D={D} keys={5 * A}")
+    with pytest.raises(tm.TMError) as e:  # one more key per frame no longer fits
+        tm.tm_audio_cross_attn_fwd(tm.make_audio_desc(B, H, D, T, A + 1, Fa, M, w), qd, 2,
+                                   akd, avd, torch.from_numpy(face).cuda())
+    assert e.value.status == tm.TM_E_SHAPE
+
+
+def test_audio_in_place_deterministic_and_empty(tm):
+    B, H, D, T, A, Fa, M, w = 1, 4, 128, 96, 32, 7, 2, 2
+    n = 3 * T
+    say("audio in place, determinism, no rows")
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(55, B, n, H, D, M, Fa * A)
+    face_np = rng.choice([-1, 0, 1], size=(B, n)).astype(np.int32)
+    face = torch.from_numpy(face_np).cuda()
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o1 = tm.tm_audio_cross_attn_fwd(desc, qd, 3, akd, avd, face)
+    o2 = tm.tm_audio_cross_attn_fwd(desc, qd, 3, akd, avd, face)
+    qq = qd.clone()
+    o3 = tm.tm_audio_cross_attn_fwd(desc, qq, 3, akd, avd, face, o=qq)
+    torch.cuda.synchronize()
+    assert o3 is qq
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(o1.view(torch.int16), qq.view(torch.int16))
+    _check(o1, q, ak, av, face_np, T, A, 3, w, "in place")
+    canary = torch.full_like(qd, 3.0)
+    tm.tm_audio_cross_attn_fwd(desc, qd, 3, akd, avd, face, o=canary, n_tok=0)
+    torch.cuda.synchronize()
+    assert bool((canary == 3.0).all())
+
+
+def test_audio_480p_two_faces_full(tm):
+    w = AUDIO_WORKLOADS["wan14b_480p_audio_2faces"]
+    say(f"audio {w.name}: {w.n_tok} rows x {w.heads} heads, frames {w.first_frame}.., two faces")
+    d = draw_audio(w)
+    desc = tm.make_audio_desc(w.batch, w.heads, w.head_dim, w.tokens_per_frame, w.audio_per_frame,
+                              w.audio_frames, w.streams, w.half_window)
+    o = tm.tm_audio_cross_attn_fwd(desc, _dev(d["q_bits"]), w.first_frame, _dev(d["ak_bits"]),
+                                   _dev(d["av_bits"]), torch.from_numpy(d["face"]).cuda())
+    torch.cuda.synchronize()
+    _check(o, d["q"], d["ak"], d["av"], d["face"], w.tokens_per_frame, w.audio_per_frame,
+           w.first_frame, w.half_window, w.name)
+
+
+def test_audio_480p_chunk_sampled(tm):
+    w = AUDIO_WORKLOADS["wan14b_480p_audio_chunk"]
+    say(f"audio {w.name}: {w.n_tok} rows x {w.heads} heads, sampled")
+    d = draw_audio(w)
+    desc = tm.make_audio_desc(w.batch, w.heads, w.head_dim, w.tokens_per_frame, w.audio_per_frame,
+                              w.audio_frames, w.streams, w.half_window)
+    o = tm.tm_audio_cross_attn_fwd(desc, _dev(d["q_bits"]), w.first_frame, _dev(d["ak_bits"]),
+                                   _dev(d["av_bits"]), torch.from_numpy(d["face"]).cuda())
+    torch.cuda.synchronize()
+    # every row without a face is zero (all heads); face rows sampled
+    on = torch.from_numpy(d["face"] >= 0).cuda()
+    assert bool((o[~on] == 0).all())
+    rng = np.random.default_rng(3)
+    face_rows = np.flatnonzero(d["face"][0] >= 0)
+    rows = np.sort(np.concatenate([rng.choice(face_rows, 160, replace=False),
+                                   rng.choice(np.flatnonzero(d["face"][0] < 0), 32, replace=False)]))
+    _check(o, d["q"], d["ak"], d["av"], d["face"], w.tokens_per_frame, w.audio_per_frame,
+           w.first_frame, w.half_window, w.name, heads=[0, 13, 39], rows=rows)
