@@ -23,6 +23,9 @@ What it computes, and where the paper defines it:
   set, used to pin ``attention`` on tiny inputs.
 * ``producer``  -- the RMS normalisation of query and key rows that precedes
   the attention and the KV cache (the fused K/V producer).
+* ``backward``  -- the gradients dQ, dK, dV of the sparse causal attention
+  (for training the student through it), from the chain rule over the
+  masked row softmax.
 * ``audio``     -- the audio cross-attention of Sec. 4.1: each latent frame's
   tokens attend to the audio tokens of the five frames centred on it, face
   tokens only, each face to its own audio stream.
@@ -47,3 +50,4 @@ from .attention import (  # noqa: F401
 from .brute import brute_force_attention  # noqa: F401
 from .producer import rms_normalise  # noqa: F401
 from .audio import audio_cross_attention, audio_window  # noqa: F401
+from .backward import masked_attention_backward, full_sequence_attention_backward  # noqa: F401
