@@ -324,8 +324,9 @@ def timing_inputs(torch, shape, seed):
 
 def other_workloads(torch, tm, workloads, stream, reps=10):
     """Attention TFLOP/s (unmasked pairs) of the 480p full sequence (21 latent
-    frames, one call over all 32760 queries) and of the 720p chunk with two
-    streams (append + attention over a cache of c_0 and the previous chunk)."""
+    frames, one call over all 32760 queries) and of its backward, of the 720p
+    chunk with two streams and of the 512x512 chunk (attention over a cache of
+    c_0 and the previous chunk)."""
     def time_call(fn):
         fn()
         torch.cuda.synchronize()
@@ -352,7 +353,21 @@ def other_workloads(torch, tm, workloads, stream, reps=10):
                    "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
                    "dense_equivalent_tflops": round(4.0 * w.head_dim * w.heads * L * L /
                                                     (ms * 1e-3) / 1e12, 2)}
-    del q, k, v, o
+    # the backward of the same call (training): delta, dQ and dK/dV kernels;
+    # 10 * head_dim FLOPs per allowed pair (S recomputed, dP, dV, dQ, dK)
+    lse = torch.empty(w.batch, w.heads, L, dtype=torch.float32, device="cuda")
+    tm.tm_sparse_causal_attn_fwd(desc, q, -1, k=k, v=v, n_frames=w.n_frames, o=o, lse=lse)
+    dout = timing_inputs(torch, (w.batch, L, w.heads, w.head_dim), 4)[2]
+    delta = torch.empty_like(lse)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ms_b = time_call(lambda: tm.tm_sparse_causal_attn_bwd(desc, w.n_frames, q, k, v, o, lse, dout,
+                                                          delta=delta, dq=dq, dk=dk, dv=dv))
+    out[w.name + "_backward"] = {"ms": round(ms_b, 4),
+                                 "tflops": round(2.5 * flops / (ms_b * 1e-3) / 1e12, 2),
+                                 "pct_bf16_peak": round(100 * 2.5 * flops / (ms_b * 1e-3) / 1e12 /
+                                                        PEAK_BF16_TFLOPS, 2),
+                                 "flop_count": "10 * head_dim per allowed pair"}
+    del q, k, v, o, lse, dout, delta, dq, dk, dv
     torch.cuda.empty_cache()
 
     # chunks over a cache of c_0 and the previous chunk: the 720p chunk with two

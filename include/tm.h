@@ -177,6 +177,25 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
                                     const tm_kv_cache* cache, const void* k, const void* v,
                                     int32_t n_frames, void* o, float* lse, hipStream_t stream);
 
+/* Backward pass of the full-sequence form (training the student through the
+ * attention of Sec. 4.2): given dO = dL/dO, the gradients
+ *   dV = P^T dO, dS = P * (dO V^T - rowsum(dO * O)), dQ = scale dS K,
+ *   dK = scale dS^T Q,
+ * with P the masked row softmax recomputed from lse. Only allowed (query, key)
+ * pairs are visited (the same tile skipping as the forward).
+ * q, k, v, o, dout: device bf16 [B, L, H, D] with L = n_frames * T, as in the
+ * full-sequence forward with q_chunk = -1 (o is its output).
+ * lse: device fp32 [B, H, L], the forward's natural-log normaliser (4-byte
+ * aligned). delta: caller-owned device fp32 workspace [B, H, L], overwritten
+ * with rowsum(dO * O). dq, dk, dv: device bf16 [B, L, H, D], every row
+ * written; they must not overlap each other or any input.
+ * TM_BF16 only (else TM_E_DTYPE). Three launches on `stream`; deterministic
+ * (no atomics). */
+tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, const void* q,
+                                    const void* k, const void* v, const void* o, const float* lse,
+                                    const void* dout, float* delta, void* dq, void* dk, void* dv,
+                                    hipStream_t stream);
+
 /* Number of allowed (query, key) pairs per (batch, head) of the call the same
  * arguments would make (4*D of FLOPs each); -1 on invalid arguments. Pure host
  * arithmetic, launches nothing; the streaming form reads the cache

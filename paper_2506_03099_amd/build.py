@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libtm.so")
 
-SOURCES = ["tm_api.cpp", "attn_fwd.hip", "kv_append.hip", "audio_attn.hip"]
+SOURCES = ["tm_api.cpp", "attn_fwd.hip", "kv_append.hip", "audio_attn.hip", "attn_bwd.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -492,6 +492,80 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
     return TM_OK;
 }
 
+tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, const void* q,
+                                    const void* k, const void* v, const void* o, const float* lse,
+                                    const void* dout, float* delta, void* dq, void* dk, void* dv,
+                                    hipStream_t stream) {
+    Geo g;
+    tm_status st = check_desc(desc, &g);
+    if (st != TM_OK) return st;
+    if (g.dtype != TM_BF16) return fail(TM_E_DTYPE, "the backward pass runs in TM_BF16 only");
+    if (n_frames < 1) return fail(TM_E_SHAPE, "n_frames must be >= 1");
+    const int64_t L = int64_t(n_frames) * g.T;
+    if (L > kMaxTokens) return fail(TM_E_SHAPE, "sequence too long (more than 2^30 tokens)");
+    const size_t t_bytes = size_t(g.B) * size_t(L) * size_t(g.H) * size_t(g.D) * 2;
+    const size_t r_bytes = size_t(g.B) * size_t(g.H) * size_t(L) * sizeof(float);
+    const void* ins[] = {q, k, v, o, dout};
+    const char* in_names[] = {"q", "k", "v", "o", "dO"};
+    for (int i = 0; i < 5; ++i)
+        if ((st = check_ptr(ins[i], t_bytes, in_names[i])) != TM_OK) return st;
+    if ((st = check_ptr(lse, r_bytes, "lse", 4)) != TM_OK) return st;
+    if ((st = check_ptr(delta, r_bytes, "delta", 4)) != TM_OK) return st;
+    void* outs[] = {dq, dk, dv};
+    const char* out_names[] = {"dq", "dk", "dv"};
+    for (int i = 0; i < 3; ++i) {
+        if ((st = check_ptr(outs[i], t_bytes, out_names[i])) != TM_OK) return st;
+        for (int j = 0; j < 5; ++j)
+            if (overlaps(outs[i], t_bytes, ins[j], t_bytes))
+                return fail(TM_E_ARG, "%s overlaps %s", out_names[i], in_names[j]);
+        if (overlaps(outs[i], t_bytes, lse, r_bytes) || overlaps(outs[i], t_bytes, delta, r_bytes))
+            return fail(TM_E_ARG, "%s overlaps lse or delta", out_names[i]);
+        for (int j = 0; j < i; ++j)
+            if (overlaps(outs[i], t_bytes, outs[j], t_bytes))
+                return fail(TM_E_ARG, "%s overlaps %s", out_names[i], out_names[j]);
+    }
+    for (int j = 0; j < 5; ++j)
+        if (overlaps(delta, r_bytes, ins[j], t_bytes))
+            return fail(TM_E_ARG, "delta overlaps %s", in_names[j]);
+    if (overlaps(delta, r_bytes, lse, r_bytes)) return fail(TM_E_ARG, "delta overlaps lse");
+
+    tmk::BwdArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.lse = lse;
+    a.dout = dout;
+    a.delta = delta;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.B = int32_t(g.B);
+    a.H = int32_t(g.H);
+    a.L = int32_t(L);
+    a.ref_tok = int32_t(g.RT);
+    a.chunk_tok = int32_t(g.CT);
+    a.window = int32_t(g.W);
+    a.scale = g.scale;
+    a.scale_log2 = float(double(g.scale) * 1.4426950408889634);
+    const int64_t nc = n_chunks(g, L);
+    const int64_t ref_rows = std::min(g.RT, L);
+    const int64_t qrt = ceil_div(ref_rows, tmk::kBwdQTile), qct = ceil_div(g.CT, tmk::kBwdQTile);
+    const int64_t krt = ceil_div(ref_rows, tmk::kBwdKTile), kct = ceil_div(g.CT, tmk::kBwdKTile);
+    const int64_t q_tiles = qrt + (nc - 1) * qct, k_tiles = krt + (nc - 1) * kct;
+    if (q_tiles * g.B * g.H > INT32_MAX || k_tiles * g.B * g.H > INT32_MAX)
+        return fail(TM_E_SHAPE, "grid too large");
+    a.q_tiles = int32_t(q_tiles);
+    a.q_ref_tiles = int32_t(qrt);
+    a.q_chunk_tiles = int32_t(qct);
+    a.k_tiles = int32_t(k_tiles);
+    a.k_ref_tiles = int32_t(krt);
+    a.k_chunk_tiles = int32_t(kct);
+    const hipError_t e = tmk::launch_attn_bwd_bf16(a, int(g.D), stream);
+    if (e != hipSuccess) return fail(TM_E_DEVICE, "backward launch: %s", hipGetErrorString(e));
+    return TM_OK;
+}
+
 tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t first_frame,
                                   int32_t n_tok, const void* ak, const void* av,
                                   const int32_t* face, void* o, hipStream_t stream) {

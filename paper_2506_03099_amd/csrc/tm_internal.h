@@ -116,4 +116,29 @@ constexpr int kAudioMaxKeys = static_cast<int>((kAudioMaxLds - kAudioFaceLds) / 
 
 hipError_t launch_audio_attn_bf16(const AudioArgs& a, int head_dim, hipStream_t s);
 
+// Backward of the whole-sequence attention (bf16): q, k, v, o, dout, dq, dk,
+// dv are [B, L, H, D]; lse (natural log) and delta (written here) are fp32
+// [B, H, L]. Query tiles of kBwdQTile rows and key tiles of kBwdKTile keys
+// never straddle a chunk: ref tiles for c_0, then chunk tiles per chunk.
+constexpr int kBwdQTile = 128;
+constexpr int kBwdKTile = 256;
+struct BwdArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const void* o;
+    const float* lse;
+    const void* dout;
+    float* delta;
+    void* dq;
+    void* dk;
+    void* dv;
+    int32_t B, H, L;
+    int32_t ref_tok, chunk_tok, window;  // R*T, C*T, W
+    float scale, scale_log2;
+    int32_t q_tiles, q_ref_tiles, q_chunk_tiles;
+    int32_t k_tiles, k_ref_tiles, k_chunk_tiles;
+};
+hipError_t launch_attn_bwd_bf16(const BwdArgs& a, int head_dim, hipStream_t s);
+
 }  // namespace tmk

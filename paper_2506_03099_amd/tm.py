@@ -105,6 +105,8 @@ def lib() -> ctypes.CDLL:
             "tm_allowed_pairs": (ctypes.c_int64, [D, ctypes.c_int32, P, ctypes.c_int32]),
             "tm_audio_cross_attn_fwd": (ctypes.c_int, [AD, P, ctypes.c_int32, ctypes.c_int32, P, P,
                                                        P, P, P]),
+            "tm_sparse_causal_attn_bwd": (ctypes.c_int, [D, ctypes.c_int32, P, P, P, P, P, P, P,
+                                                         P, P, P, P]),
             "tm_last_error": (ctypes.c_char_p, []),
         }
         for name, (res, args) in sig.items():
@@ -268,3 +270,18 @@ def tm_audio_cross_attn_fwd(desc: tm_audio_desc, q, first_frame: int, ak, av, fa
     _check(lib().tm_audio_cross_attn_fwd(ctypes.byref(desc), _ptr(q), first_frame, n_tok, _ptr(ak),
                                          _ptr(av), _ptr(face), _ptr(o), _stream(stream)))
     return o
+
+
+def tm_sparse_causal_attn_bwd(desc: tm_attn_desc, n_frames: int, q, k, v, o, lse, dout, delta=None,
+                              dq=None, dk=None, dv=None, stream=None):
+    """Gradients (dq, dk, dv) of the full-sequence sparse causal attention;
+    ``delta`` is an fp32 [B, H, L] workspace (allocated if not given)."""
+    if delta is None:
+        delta = torch.empty_like(lse)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    _check(lib().tm_sparse_causal_attn_bwd(ctypes.byref(desc), n_frames, _ptr(q), _ptr(k), _ptr(v),
+                                           _ptr(o), _ptr(lse), _ptr(dout), _ptr(delta), _ptr(dq),
+                                           _ptr(dk), _ptr(dv), _stream(stream)))
+    return dq, dk, dv

@@ -196,3 +196,21 @@ def test_audio_rejects_bad_arguments(tm):
     edge = _adesc(tm, audio_per_frame=90, audio_frames=3)  # frames 0..2: at most 3 * 90 = 270 keys
     st = L.tm_audio_cross_attn_fwd(ctypes.byref(edge), FAKE, 0, 1560, FAKE, FAKE, FAKE, FAKE, None)
     assert st == tm.TM_E_ARG
+
+
+# --------------------------------------------------------------------------- backward
+
+
+def test_backward_rejects_bad_arguments(tm):
+    L = tm.lib()
+    d = _desc(tm)
+    call = lambda desc, nf, q=FAKE, lse=FAKE: L.tm_sparse_causal_attn_bwd(
+        ctypes.byref(desc), nf, q, FAKE, FAKE, FAKE, lse, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert call(_desc(tm, dtype=tm.TM_F32), 21) == tm.TM_E_DTYPE
+    assert call(_desc(tm, head_dim=96), 21) == tm.TM_E_SHAPE
+    assert call(d, 0) == tm.TM_E_SHAPE
+    assert call(d, 21, q=None) == tm.TM_E_ARG
+    assert call(d, 21, lse=FAKE + 2) == tm.TM_E_ARG   # misaligned
+    assert call(d, 21) == tm.TM_E_ARG                 # not device memory
+    assert L.tm_sparse_causal_attn_bwd(None, 21, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                       FAKE, None) == tm.TM_E_ARG

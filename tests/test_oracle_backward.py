@@ -116,7 +116,7 @@ def test_unmutated_backward_oracle_passes():
 
 
 def _mutant(kind):
-    def f(q, k, v, do, mask, scale, *, dtype=np.float64):
+    def f(q, k, v, do, mask, scale, *, dtype=np.float64, magnitudes=False):
         q, k, v, do = (np.asarray(x, dtype=dtype) for x in (q, k, v, do))
         s = np.where(mask, (q @ k.T) * scale, -np.inf)
         e = np.where(mask, np.exp(s - s.max(axis=1, keepdims=True)), 0.0)
@@ -134,3 +134,21 @@ def _mutant(kind):
 def test_backward_mutants_fail_a_pin(monkeypatch, kind):
     monkeypatch.setattr(bwd, "masked_attention_backward", _mutant(kind))
     assert not _pins_hold()
+
+
+def test_magnitudes_bound_the_gradients():
+    # |sum x y| <= sum |x y|, with equality when all products share a sign
+    g = ChunkGeometry(4, 2, 1, 1)
+    (q, k, v, do), L = _case(9, g, 7, D=5, B=1, H=2)
+    grads, mags = bwd.full_sequence_attention_backward(q, k, v, do, g, magnitudes=True)
+    plain = bwd.full_sequence_attention_backward(q, k, v, do, g)
+    for gr, pl, mg in zip(grads, plain, mags):
+        assert np.array_equal(gr, pl)
+        assert np.all(np.abs(gr) <= mg * (1 + 1e-12) + 1e-300)
+    pos = np.arange(L)
+    mask = allowed_mask(pos, pos, g)
+    ones = np.ones((L, 5))
+    _, (_, _, mdv) = bwd.masked_attention_backward(q[0, :, 0], k[0, :, 0], v[0, :, 0], ones, mask, 0.5,
+                                                   magnitudes=True)
+    dq, dk, dv = bwd.masked_attention_backward(q[0, :, 0], k[0, :, 0], v[0, :, 0], ones, mask, 0.5)
+    assert np.allclose(mdv, dv)  # dO = 1 > 0: |P|^T |dO| = P^T dO
