@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "tm_device.h"
 #include "tm_internal.h"
 
@@ -343,15 +345,22 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
     }
 }
 
+// The kernel's dynamic-LDS limit is raised once per device (to the largest
+// size, which covers every launch); concurrent first calls set the same value.
+constexpr int kMaxDevices = 64;
+
 template <int D>
 hipError_t launch(const AudioArgs& a, unsigned grid, size_t lds, hipStream_t s) {
-    static bool attr_set = false;  // the attribute only ever takes the largest size
-    if (!attr_set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&audio_attn_bf16_kernel<D>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 static_cast<int>(kAudioMaxLds));
+    static std::atomic<bool> attr_set[kMaxDevices];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    if (!attr_set[dev].load(std::memory_order_acquire)) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&audio_attn_bf16_kernel<D>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kAudioMaxLds));
         if (e != hipSuccess) return e;
-        attr_set = true;
+        attr_set[dev].store(true, std::memory_order_release);
     }
     hipLaunchKernelGGL(audio_attn_bf16_kernel<D>, dim3(grid), dim3(kAudioThreads), lds, s, a);
     return hipGetLastError();
