@@ -16,19 +16,22 @@
 //   64-key tile staged in LDS it recomputes S^T = K Q^T and dP^T = V dO^T and
 //   accumulates dQ^T += K^T dS^T, the same operand layouts as the forward's
 //   O^T += V^T P^T with row-major V (K^T read with transposing LDS reads);
-// - bwd_dkdv_kernel: one workgroup of 8 waves per 256-key tile (32 keys per
-//   wave) of one chunk; the queries that see a key chunk c form one range
-//   (all of them for c_0, chunks c .. c+W otherwise); per 32-query tile staged
-//   in LDS it computes S = Q K^T and dP = dO V^T (one key per lane, queries in
-//   registers) and accumulates dV^T += dO^T P and dK^T += Q^T dS, with dO^T and
-//   Q^T read with transposing LDS reads. The c_0 tiles, which see every query,
-//   are dispatched first.
+// - bwd_dkdv_kernel: one workgroup of 4 waves (one per SIMD) per 256-key
+//   tile of one chunk, 64 keys per wave held in registers; the queries that
+//   see a key chunk c form one range (all of them for c_0, chunks c .. c+W
+//   otherwise); per 32-query stage, loaded straight into LDS while the
+//   previous stage computes, it forms S = Q K^T and dP = dO V^T (one key per
+//   lane) and accumulates dV^T += dO^T P and dK^T += Q^T dS, with dO^T and
+//   Q^T read with transposing LDS reads. The c_0 tiles, which see every
+//   query, are dispatched first.
 // P and dS are rounded to bf16 for the MFMAs; accumulation is fp32; results
 // are rounded to bf16 once. No atomics: the result is deterministic.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "tm_device.h"
 #include "tm_internal.h"
@@ -37,12 +40,14 @@ namespace tmk {
 namespace {
 
 constexpr int kDqThreads = 256;    // 4 waves: 128 query rows
-constexpr int kDkdvThreads = 512;  // 8 waves: 256 keys
+constexpr int kDkdvThreads = 256;  // 4 waves, one per SIMD: 256 keys
 
 typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 typedef __attribute__((address_space(3))) float lds_f32;
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 
@@ -78,6 +83,35 @@ struct TileOffsets {
             tr[2 * d + 1] = (r + 8) * ROWB + ((cc ^ lds_swizzle<D>(r + 8)) << 4) + half;
         }
     }
+};
+
+// The same offsets from three registers: with chunk 2*kk + hw (row operand)
+// and 4*d + cbase (transposed operand) the swizzle's XOR only touches the
+// chunk bits, so row[kk] = row0 ^ (kk << 5), tr[2d] = tr0 ^ (d << 6) and
+// tr[2d + 1] = (tr8 ^ (d << 6)) + 8 * ROWB. pinned() makes a stage derive
+// them anew (one XOR per use) instead of keeping 16 registers.
+template <int D>
+struct TileBases {
+    static constexpr int ROWB = D * 2;
+    uint32_t row0, tr0, tr8;
+    __device__ __forceinline__ TileBases(int lane) {
+        const int l32 = lane & 31, hw = lane >> 5;
+        row0 = l32 * ROWB + ((hw ^ lds_swizzle<D>(l32)) << 4);
+        const int grp = lane >> 4, gi = lane & 15;
+        const int r = 4 * hw + (gi >> 2);
+        const int cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
+        const int half = (gi & 1) * 8;
+        tr0 = r * ROWB + ((cbase ^ lds_swizzle<D>(r)) << 4) + half;
+        tr8 = r * ROWB + ((cbase ^ lds_swizzle<D>(r + 8)) << 4) + half;
+    }
+    __device__ __forceinline__ TileBases pinned() const {
+        TileBases t = *this;
+        asm volatile("" : "+v"(t.row0), "+v"(t.tr0), "+v"(t.tr8));
+        return t;
+    }
+    __device__ __forceinline__ uint32_t row(int kk) const { return row0 ^ (kk << 5); }
+    __device__ __forceinline__ uint32_t tr_lo(int d) const { return tr0 ^ (d << 6); }
+    __device__ __forceinline__ uint32_t tr_hi(int d) const { return (tr8 ^ (d << 6)) + 8 * ROWB; }
 };
 
 template <int D>
@@ -282,21 +316,33 @@ __global__ __launch_bounds__(kDqThreads) void bwd_dq_kernel(const BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV: per 128-key tile of one chunk, over the queries that see the chunk
+// dK, dV: per 256-key tile of one chunk, over the queries that see the chunk
 // ---------------------------------------------------------------------------
+// One wave per SIMD (512 registers per lane): each wave owns 64 keys as two
+// groups of 32 and holds their K and V fragments (the B operands of
+// S = Q K^T and dP = dO V^T) in registers for the whole kernel, and the dK^T
+// and dV^T accumulators of both groups (256 registers). Every Q or dO fragment
+// read from LDS therefore feeds two MFMAs. The 32-query stages of Q, dO, lse
+// and delta arrive by direct global->LDS loads into two alternating buffers,
+// the next stage's loads in flight during the current stage's arithmetic;
+// one barrier per stage.
 template <int D>
-__global__ __launch_bounds__(kDkdvThreads) void bwd_dkdv_kernel(const BwdArgs a) {
-    constexpr int ROWB = D * 2, KK = D / 16, DB = D / 32;
-    constexpr int BK = kBwdKTile, BQ = 32;
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * BK * ROWB + 2 * BQ * ROWB + 2 * BQ * 4];
-    lds_u8* const Ks = (lds_u8*)smem;
-    lds_u8* const Vs = Ks + BK * ROWB;
-    lds_u8* const Qs = Vs + BK * ROWB;
-    lds_u8* const Ds = Qs + BQ * ROWB;  // dO tile
-    lds_f32* const lse_s = (lds_f32*)(Ds + BQ * ROWB);
-    lds_f32* const dl_s = lse_s + BQ;
+__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(const BwdArgs a) {
+    constexpr int ROWB = D * 2, KK = D / 16, DB = D / 32, CPR = D / 8;
+    constexpr int BQ = 32;                      // queries per stage
+    constexpr int NW = kDkdvThreads / 64;       // waves
+    constexpr int TILE = BQ * ROWB;             // one tensor's stage tile in LDS
+    constexpr int STAGE = 2 * TILE;             // Q tile, then dO tile
+    constexpr int NBW = TILE / 1024 / NW;       // 1-KB direct loads per wave and tensor
+    constexpr int VEC = 2 * STAGE;              // lse and delta: 2 buffers x 64 floats each
+    static_assert(NBW >= 1 && NBW * NW * 1024 == TILE, "stage tile must split over the waves");
+    static_assert(kBwdKTile == NW * 64, "64 keys per wave");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE + 4 * 256];
+    lds_u8* const L = (lds_u8*)smem;
+    const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(L));
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31, hw = lane >> 5;
     // c_0's key tiles (every query sees them) of all heads first
     const int BH = a.B * a.H;
@@ -313,16 +359,16 @@ __global__ __launch_bounds__(kDkdvThreads) void bwd_dkdv_kernel(const BwdArgs a)
     }
     const int h = bh % a.H, b = bh / a.H;
     int chunk, k0, k1;
-    tile_rows(a, t, BK, a.k_ref_tiles, a.k_chunk_tiles, chunk, k0, k1);
+    tile_rows(a, t, kBwdKTile, a.k_ref_tiles, a.k_chunk_tiles, chunk, k0, k1);
     if (k0 >= k1) return;
-    // queries that see key chunk `chunk`
-    int qa, qb;
+    // queries [qbeg, qend) see key chunk `chunk`
+    int qbeg, qend;
     if (chunk == 0) {
-        qa = 0;
-        qb = a.L;
+        qbeg = 0;
+        qend = a.L;
     } else {
-        qa = a.ref_tok + (chunk - 1) * a.chunk_tok;
-        qb = min(a.ref_tok + (chunk + a.window) * a.chunk_tok, a.L);
+        qbeg = a.ref_tok + (chunk - 1) * a.chunk_tok;
+        qend = min(a.ref_tok + (chunk + a.window) * a.chunk_tok, a.L);
     }
 
     const int64_t st = static_cast<int64_t>(a.H) * D;
@@ -334,77 +380,160 @@ __global__ __launch_bounds__(kDkdvThreads) void bwd_dkdv_kernel(const BwdArgs a)
     const float* lse = a.lse + (static_cast<int64_t>(b) * a.H + h) * a.L;
     const float* dl = a.delta + (static_cast<int64_t>(b) * a.H + h) * a.L;
 
-    stage_rows<D, kDkdvThreads>(Ks, kg, st, k0, k1, BK, tid);
-    stage_rows<D, kDkdvThreads>(Vs, vg, st, k0, k1, BK, tid);
-
-    const TileOffsets<D> off(lane);
-    // this wave's 32 keys as the B operands of S = Q K^T and dP = dO V^T
-    const uint32_t krow = (wave * 32 + l32) * ROWB;
-    const int kswz = lds_swizzle<D>(l32);  // (wave * 32 + l32) % 16 == l32 % 16
-    f32x16_t dk[DB], dv[DB];
+    // Direct loads of the stage starting at query q0 into buffer u: rows past
+    // qend repeat row qend - 1 (finite values, masked below). Each 1-KB block
+    // holds 64 consecutive 16-byte LDS chunks of the swizzled tile; the lane
+    // whose chunk is logical chunk gc of row `row` fetches that chunk.
+    auto issue = [&](int q0, int u) __attribute__((always_inline)) {
+        const int last = qend - 1 - q0;
+        const void* qs = uniform_ptr(qg + q0 * st);
+        const void* ds = uniform_ptr(dog + q0 * st);
 #pragma unroll
-    for (int d = 0; d < DB; ++d) dk[d] = dv[d] = f32x16_t{};
-    const float c = a.scale_log2;
-
-    for (int q0 = qa; q0 < qb; q0 += BQ) {
-        __syncthreads();  // the previous query tile is no longer read (and K/V are staged)
-        stage_rows<D, kDkdvThreads>(Qs, qg, st, q0, qb, BQ, tid);
-        stage_rows<D, kDkdvThreads>(Ds, dog, st, q0, qb, BQ, tid);
-        if (tid < BQ) {
-            const int qr = min(q0 + tid, qb - 1);
-            lse_s[tid] = lse[qr] * 1.4426950408889634f;
-            dl_s[tid] = dl[qr];
+        for (int i = 0; i < NBW; ++i) {
+            const int blk = i * NW + wave;
+            const int ch = blk * 64 + lane;
+            const int row = ch / CPR;
+            const int gc = (ch % CPR) ^ lds_swizzle<D>(row);
+            const uint32_t voff = static_cast<uint32_t>((min(row, last) * st + gc * 8) * 2);
+            const uint32_t l = lds_base + u * STAGE + blk * 1024;
+            lds_dma16x2(qs, voff, l, ds, voff, l + TILE);
         }
-        __syncthreads();
-        f32x16_t s = f32x16_t{}, dp = f32x16_t{};
+        if (wave == 0) {
+            const uint32_t vo = static_cast<uint32_t>(min(lane, last) * 4);
+            lds_dma4x2(uniform_ptr(lse + q0), vo, lds_base + VEC + u * 256, uniform_ptr(dl + q0), vo,
+                       lds_base + VEC + 512 + u * 256);
+        }
+    };
+
+    // this wave's keys: group g holds keys k0 + 64 * wave + 32 * g + l32
+    const int kw = k0 + 64 * wave;
+    const bool busy = kw < k1;
+    bf16x8_t kf[2][KK], vf[2][KK];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+        const int kr = min(kw + 32 * g + l32, k1 - 1);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            const bf16x8_t qa_f = *(lds_bf16x8_t*)(Qs + off.row[kk]);
-            const bf16x8_t da_f = *(lds_bf16x8_t*)(Ds + off.row[kk]);
-            const int pos = ((2 * kk + hw) ^ kswz) << 4;
-            const bf16x8_t kb_f = *(lds_bf16x8_t*)(Ks + krow + pos);
-            const bf16x8_t vb_f = *(lds_bf16x8_t*)(Vs + krow + pos);
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa_f, kb_f, s, 0, 0, 0);
-            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da_f, vb_f, dp, 0, 0, 0);
+            kf[g][kk] = *reinterpret_cast<const bf16x8_t*>(kg + kr * st + kk * 16 + hw * 8);
+            vf[g][kk] = *reinterpret_cast<const bf16x8_t*>(vg + kr * st + kk * 16 + hw * 8);
         }
-        // register i: query 8*(i/4) + 4*hw + i%4 of the tile, key l32 of the wave
-        bf16x8_t pf[2], sf[2];
+    }
+    // the K/V loads land before any direct load is issued
+    wait_lds_dma();
+
+    const TileBases<D> tb(lane);
+    f32x16_t dk[2][DB], dv[2][DB];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int qi = 8 * (i / 4) + 4 * hw + (i % 4);
-            const float p = q0 + qi < qb ? __builtin_amdgcn_exp2f(fmaf(s[i], c, -lse_s[qi])) : 0.f;
-            pf[i / 8][i % 8] = static_cast<__bf16>(p);
-            sf[i / 8][i % 8] = static_cast<__bf16>(p * (dp[i] - dl_s[qi]));
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int d = 0; d < DB; ++d) dk[g][d] = dv[g][d] = f32x16_t{};
+    const float c = a.scale_log2;
+
+    // One stage from buffer U: S = Q K^T and dP = dO V^T (register i of a
+    // group: query 8*(i/4) + 4*hw + i%4 of the stage, key l32 of the group),
+    // then dV^T += dO^T P and dK^T += Q^T dS over the stage's 32 queries.
+    auto compute = [&](auto ucst, int q0) __attribute__((always_inline)) {
+        constexpr int U = decltype(ucst)::value;
+        const lds_u8* Qb = L + U * STAGE;
+        const lds_u8* Db = Qb + TILE;
+        const lds_f32* ls = (const lds_f32*)(L + VEC + U * 256);
+        const lds_f32* dls = (const lds_f32*)(L + VEC + 512 + U * 256);
+        const TileBases<D> off = tb.pinned();
+        f32x16_t s[2] = {f32x16_t{}, f32x16_t{}}, dp[2] = {f32x16_t{}, f32x16_t{}};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8_t qa = *(const lds_bf16x8_t*)(Qb + off.row(kk));
+            s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[0][kk], s[0], 0, 0, 0);
+            s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[1][kk], s[1], 0, 0, 0);
         }
-        // dV^T += dO^T P and dK^T += Q^T dS, over the tile's 32 queries (2 k-steps)
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const bf16x8_t da = *(const lds_bf16x8_t*)(Db + off.row(kk));
+            dp[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[0][kk], dp[0], 0, 0, 0);
+            dp[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[1][kk], dp[1], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // P and dS of one key group, then the other, 4 consecutive queries at
+        // a time: their log2-scaled lse (+inf for rows past qend, so that
+        // P = 0) and delta
+        const int rows = qend - q0;
+        bf16x8_t pf[2][2], sf[2][2];
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int q4 = 8 * g4 + 4 * hw;
+                const f32x4_t x = *(const lds_f32x4_t*)(ls + q4);
+                const f32x4_t y = *(const lds_f32x4_t*)(dls + q4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = 4 * g4 + e;
+                    const float ml = q4 + e < rows ? x[e] * 1.4426950408889634f : __builtin_inff();
+                    const float p = __builtin_amdgcn_exp2f(fmaf(s[g][i], c, -ml));
+                    pf[g][i / 8][i % 8] = static_cast<__bf16>(p);
+                    sf[g][i / 8][i % 8] = static_cast<__bf16>(p * (dp[g][i] - y[e]));
+                }
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
 #pragma unroll
             for (int d = 0; d < DB; ++d) {
-                const bf16x8_t dt = read_tr<D>(Ds + 16 * j * ROWB, off.tr[2 * d], off.tr[2 * d + 1]);
-                const bf16x8_t qt = read_tr<D>(Qs + 16 * j * ROWB, off.tr[2 * d], off.tr[2 * d + 1]);
-                dv[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dt, pf[j], dv[d], 0, 0, 0);
-                dk[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qt, sf[j], dk[d], 0, 0, 0);
+                const bf16x8_t dt = read_tr<D>(Db + 16 * j * ROWB, off.tr_lo(d), off.tr_hi(d));
+                dv[0][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dt, pf[0][j], dv[0][d], 0, 0, 0);
+                dv[1][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dt, pf[1][j], dv[1][d], 0, 0, 0);
             }
         }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+                const bf16x8_t qt = read_tr<D>(Qb + 16 * j * ROWB, off.tr_lo(d), off.tr_hi(d));
+                dk[0][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qt, sf[0][j], dk[0][d], 0, 0, 0);
+                dk[1][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qt, sf[1][j], dk[1][d], 0, 0, 0);
+            }
+        }
+    };
+
+    const int n_st = (qend - qbeg + BQ - 1) / BQ;
+    issue(qbeg, 0);
+    wait_lds_dma();
+    __syncthreads();
+    for (int ts = 0; ts < n_st; ts += 2) {
+        const int q0 = qbeg + ts * BQ;
+        // buffer 1 was last read in the previous stage, before the barrier
+        if (ts + 1 < n_st) issue(q0 + BQ, 1);
+        if (busy) compute(std::integral_constant<int, 0>{}, q0);
+        wait_lds_dma();
+        __syncthreads();
+        if (ts + 1 >= n_st) break;
+        if (ts + 2 < n_st) issue(q0 + 2 * BQ, 0);
+        if (busy) compute(std::integral_constant<int, 1>{}, q0 + BQ);
+        wait_lds_dma();
+        __syncthreads();
     }
-    const int key = k0 + wave * 32 + l32;
-    if (key < k1) {
-        __bf16* dkp = static_cast<__bf16*>(a.dk) + base + key * st;
-        __bf16* dvp = static_cast<__bf16*>(a.dv) + base + key * st;
-        const float sc = a.scale;
+
+    const float sc = a.scale;
 #pragma unroll
-        for (int d = 0; d < DB; ++d) {
+    for (int g = 0; g < 2; ++g) {
+        const int key = kw + 32 * g + l32;
+        if (key < k1) {
+            __bf16* dkp = static_cast<__bf16*>(a.dk) + base + key * st;
+            __bf16* dvp = static_cast<__bf16*>(a.dv) + base + key * st;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                bf16x4_t wk, wv;
+            for (int d = 0; d < DB; ++d) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    wk[e] = static_cast<__bf16>(dk[d][4 * g + e] * sc);
-                    wv[e] = static_cast<__bf16>(dv[d][4 * g + e]);
+                for (int q = 0; q < 4; ++q) {
+                    bf16x4_t wk, wv;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        wk[e] = static_cast<__bf16>(dk[g][d][4 * q + e] * sc);
+                        wv[e] = static_cast<__bf16>(dv[g][d][4 * q + e]);
+                    }
+                    *reinterpret_cast<bf16x4_t*>(dkp + 32 * d + 8 * q + 4 * hw) = wk;
+                    *reinterpret_cast<bf16x4_t*>(dvp + 32 * d + 8 * q + 4 * hw) = wv;
                 }
-                *reinterpret_cast<bf16x4_t*>(dkp + 32 * d + 8 * g + 4 * hw) = wk;
-                *reinterpret_cast<bf16x4_t*>(dvp + 32 * d + 8 * g + 4 * hw) = wv;
             }
         }
     }

@@ -51,48 +51,6 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 // Threads per workgroup of the bf16 kernel: 8 waves (two per SIMD) sharing
 // every K/V tile staged in LDS.
 constexpr int kBf16Threads = 512;
-// s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
-constexpr int kWaitVmcnt0 = 0x0F70;
-
-// A pointer that is the same in every lane, held in scalar registers.
-__device__ __forceinline__ const void* uniform_ptr(const void* p) {
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
-    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
-    return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
-}
-
-// Two direct global->LDS loads (global_load_lds_dwordx4) of 16 bytes per lane:
-// load n reads from the wave-uniform base sbase<n> plus the lane's byte offset
-// voff<n>, and lane l's bytes land at LDS address lds<n> + 16 * l. The LDS
-// address goes through M0 (saved and restored); an SALU write of M0 needs one
-// wait state before an LDS-DMA instruction (or anything else) reads it, hence
-// the s_nop after each write. Written as inline assembly so that these loads
-// stay out of the compiler's wait bookkeeping, which would otherwise make LDS
-// reads of one tile wait for the loads of later tiles; the kernel waits for
-// them explicitly before the barrier that publishes a tile.
-__device__ __forceinline__ void lds_dma16x2(const void* sbase0, uint32_t voff0, uint32_t lds0,
-                                            const void* sbase1, uint32_t voff1, uint32_t lds1) {
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %2, %3\n\t"
-        "s_mov_b32 m0, %4\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %5, %6\n\t"
-        "s_mov_b32 m0, %0\n\t"
-        "s_nop 0"
-        : "=&s"(saved)
-        : "s"(lds0), "v"(voff0), "s"(sbase0), "s"(lds1), "v"(voff1), "s"(sbase1));
-}
-
-// Wait until every direct global->LDS load issued by this wave has written
-// LDS. The barrier that publishes a tile only orders LDS operations; the
-// direct loads count as vector-memory operations, so each wave waits for its
-// own before the barrier, and after the barrier the whole tile is in place.
-__device__ __forceinline__ void wait_lds_dma() { __builtin_amdgcn_s_waitcnt(kWaitVmcnt0); }
 // Wait until at most N LDS operations (and scalar loads) of this wave are
 // outstanding; vector-memory and export counts are left unconstrained.
 template <int N>
