@@ -16,14 +16,14 @@
 //   64-key tile staged in LDS it recomputes S^T = K Q^T and dP^T = V dO^T and
 //   accumulates dQ^T += K^T dS^T, the same operand layouts as the forward's
 //   O^T += V^T P^T with row-major V (K^T read with transposing LDS reads);
-// - bwd_dkdv_kernel: one workgroup of 4 waves (one per SIMD) per 256-key
-//   tile of one chunk, 64 keys per wave held in registers; the queries that
-//   see a key chunk c form one range (all of them for c_0, chunks c .. c+W
-//   otherwise); per 32-query stage, loaded straight into LDS while the
-//   previous stage computes, it forms S = Q K^T and dP = dO V^T (one key per
-//   lane) and accumulates dV^T += dO^T P and dK^T += Q^T dS, with dO^T and
-//   Q^T read with transposing LDS reads. The c_0 tiles, which see every
-//   query, are dispatched first.
+// - bwd_dkdv_kernel: one workgroup of 4 waves per 128-key tile of one chunk
+//   (two workgroups share a CU, so each SIMD runs two independent waves);
+//   the queries that see a key chunk c form one range (all of them for c_0,
+//   chunks c .. c+W otherwise); per 32-query stage, loaded straight into LDS
+//   while the previous stage computes, it forms S = Q K^T and dP = dO V^T
+//   (one key per lane) and accumulates dV^T += dO^T P and dK^T += Q^T dS,
+//   with dO^T and Q^T read with transposing LDS reads. The c_0 tiles, which
+//   see every query, are dispatched first.
 // P and dS are rounded to bf16 for the MFMAs; accumulation is fp32; results
 // are rounded to bf16 once. No atomics: the result is deterministic.
 
@@ -40,7 +40,7 @@ namespace tmk {
 namespace {
 
 constexpr int kDqThreads = 256;    // 4 waves: 128 query rows
-constexpr int kDkdvThreads = 256;  // 4 waves, one per SIMD: 256 keys
+constexpr int kDkdvThreads = 256;  // 4 waves: 128 keys; two workgroups per CU
 
 typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
 typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
@@ -85,6 +85,18 @@ struct TileOffsets {
     }
 };
 
+// Position of 16-byte chunk c of row `row` in a Q, dO or V tile of the dK/dV
+// kernel: c ^ bwd_swizzle<D>(row). LDS serves 64 banks of 4 bytes: a 16-byte
+// read per lane covers 16 lanes per cycle (16 consecutive rows of one chunk:
+// distinct chunk slots), an 8-byte transposing read 32 lanes (4 consecutive
+// rows, 4 chunks each: distinct 64-byte slot groups). D = 128: a permutation
+// of 0..15 over 16 rows whose bits 2-3 differ over 4 aligned rows; D = 64
+// (two rows per 256 bytes): the same within the even and within the odd rows.
+template <int D>
+__device__ __forceinline__ int bwd_swizzle(int row) {
+    return D == 128 ? 4 * (row & 3) + ((row >> 2) & 3) : 4 * ((row >> 1) & 1) + ((row >> 2) & 3);
+}
+
 // The same offsets from three registers: with chunk 2*kk + hw (row operand)
 // and 4*d + cbase (transposed operand) the swizzle's XOR only touches the
 // chunk bits, so row[kk] = row0 ^ (kk << 5), tr[2d] = tr0 ^ (d << 6) and
@@ -96,13 +108,13 @@ struct TileBases {
     uint32_t row0, tr0, tr8;
     __device__ __forceinline__ TileBases(int lane) {
         const int l32 = lane & 31, hw = lane >> 5;
-        row0 = l32 * ROWB + ((hw ^ lds_swizzle<D>(l32)) << 4);
+        row0 = l32 * ROWB + ((hw ^ bwd_swizzle<D>(l32)) << 4);
         const int grp = lane >> 4, gi = lane & 15;
         const int r = 4 * hw + (gi >> 2);
         const int cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
         const int half = (gi & 1) * 8;
-        tr0 = r * ROWB + ((cbase ^ lds_swizzle<D>(r)) << 4) + half;
-        tr8 = r * ROWB + ((cbase ^ lds_swizzle<D>(r + 8)) << 4) + half;
+        tr0 = r * ROWB + ((cbase ^ bwd_swizzle<D>(r)) << 4) + half;
+        tr8 = r * ROWB + ((cbase ^ bwd_swizzle<D>(r + 8)) << 4) + half;
     }
     __device__ __forceinline__ TileBases pinned() const {
         TileBases t = *this;
@@ -316,28 +328,28 @@ __global__ __launch_bounds__(kDqThreads) void bwd_dq_kernel(const BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV: per 256-key tile of one chunk, over the queries that see the chunk
+// dK, dV: per 128-key tile of one chunk, over the queries that see the chunk
 // ---------------------------------------------------------------------------
-// One wave per SIMD (512 registers per lane): each wave owns 64 keys as two
-// groups of 32 and holds their K and V fragments (the B operands of
-// S = Q K^T and dP = dO V^T) in registers for the whole kernel, and the dK^T
-// and dV^T accumulators of both groups (256 registers). Every Q or dO fragment
-// read from LDS therefore feeds two MFMAs. The 32-query stages of Q, dO, lse
-// and delta arrive by direct global->LDS loads into two alternating buffers,
-// the next stage's loads in flight during the current stage's arithmetic;
-// one barrier per stage.
+// Each wave owns 32 keys and holds their K fragments (the B operand of
+// S = Q K^T) and their dK^T and dV^T accumulators in registers (about 240 per
+// lane, so two waves fit on a SIMD); the workgroup's V rows (the B operand of
+// dP = dO V^T) sit in LDS. The 32-query stages of Q, dO, lse and delta arrive
+// by direct global->LDS loads into two alternating buffers, the next stage's
+// loads in flight during the current stage's arithmetic; one barrier per
+// stage. Two workgroups per CU keep the SIMDs' two waves out of step, so one
+// wave's softmax arithmetic overlaps the other's MFMAs.
 template <int D>
-__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(const BwdArgs a) {
+__global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs a) {
     constexpr int ROWB = D * 2, KK = D / 16, DB = D / 32, CPR = D / 8;
     constexpr int BQ = 32;                      // queries per stage
     constexpr int NW = kDkdvThreads / 64;       // waves
     constexpr int TILE = BQ * ROWB;             // one tensor's stage tile in LDS
     constexpr int STAGE = 2 * TILE;             // Q tile, then dO tile
-    constexpr int NBW = TILE / 1024 / NW;       // 1-KB direct loads per wave and tensor
+    constexpr int NB = TILE / 1024;             // 1-KB direct loads per tensor and stage
     constexpr int VEC = 2 * STAGE;              // lse and delta: 2 buffers x 64 floats each
-    static_assert(NBW >= 1 && NBW * NW * 1024 == TILE, "stage tile must split over the waves");
-    static_assert(kBwdKTile == NW * 64, "64 keys per wave");
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE + 4 * 256];
+    constexpr int VT = VEC + 4 * 256;           // V rows of the workgroup's keys
+    static_assert(kBwdKTile == NW * 32, "32 keys per wave");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[VT + kBwdKTile * ROWB];
     lds_u8* const L = (lds_u8*)smem;
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(L));
 
@@ -388,110 +400,106 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(const BwdArgs
         const int last = qend - 1 - q0;
         const void* qs = uniform_ptr(qg + q0 * st);
         const void* ds = uniform_ptr(dog + q0 * st);
-#pragma unroll
-        for (int i = 0; i < NBW; ++i) {
-            const int blk = i * NW + wave;
+        for (int blk = wave; blk < NB; blk += NW) {
             const int ch = blk * 64 + lane;
             const int row = ch / CPR;
-            const int gc = (ch % CPR) ^ lds_swizzle<D>(row);
+            const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
             const uint32_t voff = static_cast<uint32_t>((min(row, last) * st + gc * 8) * 2);
             const uint32_t l = lds_base + u * STAGE + blk * 1024;
             lds_dma16x2(qs, voff, l, ds, voff, l + TILE);
         }
-        if (wave == 0) {
+        if (wave == NW - 1) {
             const uint32_t vo = static_cast<uint32_t>(min(lane, last) * 4);
             lds_dma4x2(uniform_ptr(lse + q0), vo, lds_base + VEC + u * 256, uniform_ptr(dl + q0), vo,
                        lds_base + VEC + 512 + u * 256);
         }
     };
 
-    // this wave's keys: group g holds keys k0 + 64 * wave + 32 * g + l32
-    const int kw = k0 + 64 * wave;
+    // this wave's keys: k0 + 32 * wave + l32
+    const int kw = k0 + 32 * wave;
     const bool busy = kw < k1;
-    bf16x8_t kf[2][KK], vf[2][KK];
+    bf16x8_t kf[KK];
+    {
+        const int kr = min(kw + l32, k1 - 1);
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-        const int kr = min(kw + 32 * g + l32, k1 - 1);
+        for (int kk = 0; kk < KK; ++kk)
+            kf[kk] = *reinterpret_cast<const bf16x8_t*>(kg + kr * st + kk * 16 + hw * 8);
+    }
+    // this wave's 32 V rows into LDS (rows past k1 repeat row k1 - 1)
+    {
+        const int vk = min(kw, k1 - 1);
+        const void* vs = uniform_ptr(vg + static_cast<int64_t>(vk) * st);
+        const int vlast = k1 - 1 - vk;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            kf[g][kk] = *reinterpret_cast<const bf16x8_t*>(kg + kr * st + kk * 16 + hw * 8);
-            vf[g][kk] = *reinterpret_cast<const bf16x8_t*>(vg + kr * st + kk * 16 + hw * 8);
+        for (int i = 0; i < 32 * ROWB / 1024; i += 2) {
+            uint32_t vo[2];
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+                const int ch = (i + m) * 64 + lane;
+                const int row = ch / CPR;
+                const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
+                vo[m] = static_cast<uint32_t>((min(row, vlast) * st + gc * 8) * 2);
+            }
+            const uint32_t l = lds_base + VT + wave * 32 * ROWB + i * 1024;
+            lds_dma16x2(vs, vo[0], l, vs, vo[1], l + 1024);
         }
     }
-    // the K/V loads land before any direct load is issued
+    // the K loads and the V rows land before any stage load is issued
     wait_lds_dma();
 
     const TileBases<D> tb(lane);
-    f32x16_t dk[2][DB], dv[2][DB];
+    f32x16_t dk[DB], dv[DB];
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-        for (int d = 0; d < DB; ++d) dk[g][d] = dv[g][d] = f32x16_t{};
+    for (int d = 0; d < DB; ++d) dk[d] = dv[d] = f32x16_t{};
     const float c = a.scale_log2;
 
-    // One stage from buffer U: S = Q K^T and dP = dO V^T (register i of a
-    // group: query 8*(i/4) + 4*hw + i%4 of the stage, key l32 of the group),
-    // then dV^T += dO^T P and dK^T += Q^T dS over the stage's 32 queries.
+    // One stage from buffer U: S = Q K^T and dP = dO V^T (register i: query
+    // 8*(i/4) + 4*hw + i%4 of the stage, key l32 of the wave), then
+    // dV^T += dO^T P and dK^T += Q^T dS over the stage's 32 queries.
     auto compute = [&](auto ucst, int q0) __attribute__((always_inline)) {
         constexpr int U = decltype(ucst)::value;
         const lds_u8* Qb = L + U * STAGE;
         const lds_u8* Db = Qb + TILE;
+        const lds_u8* Vw = L + VT + wave * 32 * ROWB;
         const lds_f32* ls = (const lds_f32*)(L + VEC + U * 256);
         const lds_f32* dls = (const lds_f32*)(L + VEC + 512 + U * 256);
         const TileBases<D> off = tb.pinned();
-        f32x16_t s[2] = {f32x16_t{}, f32x16_t{}}, dp[2] = {f32x16_t{}, f32x16_t{}};
+        f32x16_t s = f32x16_t{}, dp = f32x16_t{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8_t qa = *(const lds_bf16x8_t*)(Qb + off.row(kk));
-            s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[0][kk], s[0], 0, 0, 0);
-            s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[1][kk], s[1], 0, 0, 0);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[kk], s, 0, 0, 0);
         }
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8_t da = *(const lds_bf16x8_t*)(Db + off.row(kk));
-            dp[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[0][kk], dp[0], 0, 0, 0);
-            dp[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vf[1][kk], dp[1], 0, 0, 0);
+            const bf16x8_t vb = *(const lds_bf16x8_t*)(Vw + off.row(kk));
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
         }
-        __builtin_amdgcn_sched_barrier(0);
-        // P and dS of one key group, then the other, 4 consecutive queries at
-        // a time: their log2-scaled lse (+inf for rows past qend, so that
-        // P = 0) and delta
         const int rows = qend - q0;
-        bf16x8_t pf[2][2], sf[2][2];
+        bf16x8_t pf[2], sf[2];
 #pragma unroll
-        for (int g = 0; g < 2; ++g) {
+        for (int g4 = 0; g4 < 4; ++g4) {
+            const int q4 = 8 * g4 + 4 * hw;
+            const f32x4_t x = *(const lds_f32x4_t*)(ls + q4);
+            const f32x4_t y = *(const lds_f32x4_t*)(dls + q4);
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-                const int q4 = 8 * g4 + 4 * hw;
-                const f32x4_t x = *(const lds_f32x4_t*)(ls + q4);
-                const f32x4_t y = *(const lds_f32x4_t*)(dls + q4);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int i = 4 * g4 + e;
-                    const float ml = q4 + e < rows ? x[e] * 1.4426950408889634f : __builtin_inff();
-                    const float p = __builtin_amdgcn_exp2f(fmaf(s[g][i], c, -ml));
-                    pf[g][i / 8][i % 8] = static_cast<__bf16>(p);
-                    sf[g][i / 8][i % 8] = static_cast<__bf16>(p * (dp[g][i] - y[e]));
-                }
+            for (int e = 0; e < 4; ++e) {
+                const int i = 4 * g4 + e;
+                const float ml = q4 + e < rows ? x[e] * 1.4426950408889634f : __builtin_inff();
+                const float p = __builtin_amdgcn_exp2f(fmaf(s[i], c, -ml));
+                pf[i / 8][i % 8] = static_cast<__bf16>(p);
+                sf[i / 8][i % 8] = static_cast<__bf16>(p * (dp[i] - y[e]));
             }
         }
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
 #pragma unroll
             for (int d = 0; d < DB; ++d) {
                 const bf16x8_t dt = read_tr<D>(Db + 16 * j * ROWB, off.tr_lo(d), off.tr_hi(d));
-                dv[0][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dt, pf[0][j], dv[0][d], 0, 0, 0);
-                dv[1][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dt, pf[1][j], dv[1][d], 0, 0, 0);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-#pragma unroll
-            for (int d = 0; d < DB; ++d) {
+                dv[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dt, pf[j], dv[d], 0, 0, 0);
                 const bf16x8_t qt = read_tr<D>(Qb + 16 * j * ROWB, off.tr_lo(d), off.tr_hi(d));
-                dk[0][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qt, sf[0][j], dk[0][d], 0, 0, 0);
-                dk[1][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qt, sf[1][j], dk[1][d], 0, 0, 0);
+                dk[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qt, sf[j], dk[d], 0, 0, 0);
             }
         }
     };
@@ -502,7 +510,6 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(const BwdArgs
     __syncthreads();
     for (int ts = 0; ts < n_st; ts += 2) {
         const int q0 = qbeg + ts * BQ;
-        // buffer 1 was last read in the previous stage, before the barrier
         if (ts + 1 < n_st) issue(q0 + BQ, 1);
         if (busy) compute(std::integral_constant<int, 0>{}, q0);
         wait_lds_dma();
@@ -515,25 +522,22 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(const BwdArgs
     }
 
     const float sc = a.scale;
+    const int key = kw + l32;
+    if (key < k1) {
+        __bf16* dkp = static_cast<__bf16*>(a.dk) + base + key * st;
+        __bf16* dvp = static_cast<__bf16*>(a.dv) + base + key * st;
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-        const int key = kw + 32 * g + l32;
-        if (key < k1) {
-            __bf16* dkp = static_cast<__bf16*>(a.dk) + base + key * st;
-            __bf16* dvp = static_cast<__bf16*>(a.dv) + base + key * st;
+        for (int d = 0; d < DB; ++d) {
 #pragma unroll
-            for (int d = 0; d < DB; ++d) {
+            for (int q = 0; q < 4; ++q) {
+                bf16x4_t wk, wv;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    bf16x4_t wk, wv;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        wk[e] = static_cast<__bf16>(dk[g][d][4 * q + e] * sc);
-                        wv[e] = static_cast<__bf16>(dv[g][d][4 * q + e]);
-                    }
-                    *reinterpret_cast<bf16x4_t*>(dkp + 32 * d + 8 * q + 4 * hw) = wk;
-                    *reinterpret_cast<bf16x4_t*>(dvp + 32 * d + 8 * q + 4 * hw) = wv;
+                for (int e = 0; e < 4; ++e) {
+                    wk[e] = static_cast<__bf16>(dk[d][4 * q + e] * sc);
+                    wv[e] = static_cast<__bf16>(dv[d][4 * q + e]);
                 }
+                *reinterpret_cast<bf16x4_t*>(dkp + 32 * d + 8 * q + 4 * hw) = wk;
+                *reinterpret_cast<bf16x4_t*>(dvp + 32 * d + 8 * q + 4 * hw) = wv;
             }
         }
     }

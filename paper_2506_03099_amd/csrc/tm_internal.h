@@ -121,7 +121,7 @@ hipError_t launch_audio_attn_bf16(const AudioArgs& a, int head_dim, hipStream_t 
 // [B, H, L]. Query tiles of kBwdQTile rows and key tiles of kBwdKTile keys
 // never straddle a chunk: ref tiles for c_0, then chunk tiles per chunk.
 constexpr int kBwdQTile = 128;
-constexpr int kBwdKTile = 256;
+constexpr int kBwdKTile = 128;
 struct BwdArgs {
     const void* q;
     const void* k;
