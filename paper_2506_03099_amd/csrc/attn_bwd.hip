@@ -13,8 +13,9 @@
 // - bwd_delta_kernel: delta [B, H, L] in fp32;
 // - bwd_dq_kernel: one workgroup of 4 waves per 128-row query tile (tiles
 //   never straddle a chunk, so a tile's rows share their key ranges); per
-//   64-key tile staged in LDS it recomputes S^T = K Q^T and dP^T = V dO^T and
-//   accumulates dQ^T += K^T dS^T, the same operand layouts as the forward's
+//   64-key tile, loaded straight into LDS while the previous tile computes,
+//   it recomputes S^T = K Q^T and dP^T = V dO^T and accumulates
+//   dQ^T += K^T dS^T, the same operand layouts as the forward's
 //   O^T += V^T P^T with row-major V (K^T read with transposing LDS reads);
 // - bwd_dkdv_kernel: one workgroup of 4 waves per 128-key tile of one chunk
 //   (two workgroups share a CU, so each SIMD runs two independent waves);
@@ -39,7 +40,7 @@
 namespace tmk {
 namespace {
 
-constexpr int kDqThreads = 256;    // 4 waves: 128 query rows
+constexpr int kDqThreads = 256;    // 4 waves: 128 query rows; two workgroups per CU
 constexpr int kDkdvThreads = 256;  // 4 waves: 128 keys; two workgroups per CU
 
 typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
@@ -48,60 +49,34 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 typedef __attribute__((address_space(3))) float lds_f32;
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 
-// Per-lane LDS byte offsets inside a row-major tile of D bf16 per row whose
-// 16-byte chunks are swizzled by lds_swizzle (rows at multiples of 16 keep
-// the pattern):
-// - row operand (A of S^T = K Q^T, or A of S = Q K^T): row l32, chunk
-//   2*kk + hw, for k-step kk;
-// - transposed operand (A of O^T += X^T P^T over 16 rows per step): two
-//   transposing reads of rows 4*hw + gi/4 and + 8, element columns
-//   32*d + 16*(grp & 1) + 4*(gi & 3); with these the MFMA's k index e of a
-//   lane runs over rows 4*hw + e%4 + 8*(e/4), matching the natural output
-//   layout of the first product (register i of a lane: row 8*(i/4) + 4*hw + i%4).
-template <int D>
-struct TileOffsets {
-    static constexpr int ROWB = D * 2;
-    static constexpr int KK = D / 16;
-    static constexpr int DB = D / 32;
-    uint32_t row[KK];
-    uint32_t tr[2 * DB];
-    __device__ __forceinline__ TileOffsets(int lane) {
-        const int l32 = lane & 31, hw = lane >> 5;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) row[kk] = l32 * ROWB + (((2 * kk + hw) ^ lds_swizzle<D>(l32)) << 4);
-        const int grp = lane >> 4, gi = lane & 15;
-        const int r = 4 * hw + (gi >> 2);
-        const int cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
-        const int half = (gi & 1) * 8;
-#pragma unroll
-        for (int d = 0; d < DB; ++d) {
-            const int cc = 4 * d + cbase;
-            tr[2 * d] = r * ROWB + ((cc ^ lds_swizzle<D>(r)) << 4) + half;
-            tr[2 * d + 1] = (r + 8) * ROWB + ((cc ^ lds_swizzle<D>(r + 8)) << 4) + half;
-        }
-    }
-};
-
-// Position of 16-byte chunk c of row `row` in a Q, dO or V tile of the dK/dV
-// kernel: c ^ bwd_swizzle<D>(row). LDS serves 64 banks of 4 bytes: a 16-byte
-// read per lane covers 16 lanes per cycle (16 consecutive rows of one chunk:
-// distinct chunk slots), an 8-byte transposing read 32 lanes (4 consecutive
-// rows, 4 chunks each: distinct 64-byte slot groups). D = 128: a permutation
-// of 0..15 over 16 rows whose bits 2-3 differ over 4 aligned rows; D = 64
-// (two rows per 256 bytes): the same within the even and within the odd rows.
+// Position of 16-byte chunk c of row `row` in the LDS tiles of both gradient
+// kernels (K and V in dQ; Q, dO and V in dK/dV): c ^ bwd_swizzle<D>(row).
+// LDS serves 64 banks of 4 bytes: a 16-byte read per lane covers 16 lanes per
+// cycle (16 consecutive rows of one chunk: distinct chunk slots), an 8-byte
+// transposing read 32 lanes (4 consecutive rows, 4 chunks each: distinct
+// 64-byte slot groups). D = 128: a permutation of 0..15 over 16 rows whose
+// bits 2-3 differ over 4 aligned rows; D = 64 (two rows per 256 bytes): the
+// same within the even and within the odd rows.
 template <int D>
 __device__ __forceinline__ int bwd_swizzle(int row) {
     return D == 128 ? 4 * (row & 3) + ((row >> 2) & 3) : 4 * ((row >> 1) & 1) + ((row >> 2) & 3);
 }
 
-// The same offsets from three registers: with chunk 2*kk + hw (row operand)
-// and 4*d + cbase (transposed operand) the swizzle's XOR only touches the
-// chunk bits, so row[kk] = row0 ^ (kk << 5), tr[2d] = tr0 ^ (d << 6) and
-// tr[2d + 1] = (tr8 ^ (d << 6)) + 8 * ROWB. pinned() makes a stage derive
-// them anew (one XOR per use) instead of keeping 16 registers.
+// Per-lane LDS byte offsets inside such a tile (rows at multiples of 16 keep
+// the pattern):
+// - row operand (A of S^T = K Q^T, or A of S = Q K^T): row l32, chunk
+//   2*kk + hw, for k-step kk: row(kk);
+// - transposed operand (A of X^T-times-P products over 16 rows per step):
+//   two transposing reads, tr_lo(d) and tr_hi(d), of rows 4*hw + gi/4 and
+//   + 8 at element columns 32*d + 16*(grp & 1) + 4*(gi & 3); with these the
+//   MFMA's k index e of a lane runs over rows 4*hw + e%4 + 8*(e/4), matching
+//   the natural output layout of the first product (register i of a lane:
+//   row 8*(i/4) + 4*hw + i%4).
+// The chunk is 2*kk + hw or 4*d + cbase, and the swizzle's XOR only touches
+// the chunk bits, so row(kk) = row0 ^ (kk << 5) and tr_lo(d) = tr0 ^ (d << 6):
+// three registers instead of sixteen. pinned() makes a stage derive them anew
+// (one XOR per use) rather than have the compiler keep all of them.
 template <int D>
 struct TileBases {
     static constexpr int ROWB = D * 2;
@@ -131,21 +106,6 @@ __device__ __forceinline__ bf16x8_t read_tr(const lds_u8* tile, uint32_t lo, uin
     const bf16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + lo));
     const bf16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + hi));
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// Copy `rows` rows (token stride st elements) starting at global row r0 into
-// a swizzled LDS tile of n_rows rows; rows at or past r_end repeat row
-// r_end - 1 (finite values; callers mask them).
-template <int D, int NT>
-__device__ __forceinline__ void stage_rows(lds_u8* tile, const __bf16* src, int64_t st, int r0,
-                                           int r_end, int n_rows, int tid) {
-    constexpr int CPR = D / 8;
-    for (int i = tid; i < n_rows * CPR; i += NT) {
-        const int r = i / CPR, ch = i % CPR;
-        const int gr = min(r0 + r, r_end - 1);
-        const u32x4_t x = *reinterpret_cast<const u32x4_t*>(src + gr * st + ch * 8);
-        *(lds_u32x4_t*)(tile + r * (D * 2) + ((ch ^ lds_swizzle<D>(r)) << 4)) = x;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -225,15 +185,28 @@ __device__ __forceinline__ void tile_rows(const BwdArgs& a, int t, int BM, int r
 // ---------------------------------------------------------------------------
 // dQ: per 128-row query tile, over its key ranges in 64-key tiles
 // ---------------------------------------------------------------------------
+// Each wave owns 32 query rows and holds their Q and dO fragments (the B
+// operands of S^T = K Q^T and dP^T = V dO^T) and their dQ^T accumulators in
+// registers. The key tiles of the tile's (at most two) key ranges form one
+// sequence; each tile's K and V rows arrive by direct global->LDS loads into
+// two alternating buffers, the next tile's loads in flight during the current
+// tile's arithmetic; one barrier per tile.
 template <int D>
-__global__ __launch_bounds__(kDqThreads) void bwd_dq_kernel(const BwdArgs a) {
-    constexpr int ROWB = D * 2, KK = D / 16, DB = D / 32;
+__global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(const BwdArgs a) {
+    constexpr int ROWB = D * 2, KK = D / 16, DB = D / 32, CPR = D / 8;
     constexpr int BM = kBwdQTile, BN = 64;
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * BN * ROWB];
-    lds_u8* const Ks = (lds_u8*)smem;
-    lds_u8* const Vs = Ks + BN * ROWB;
+    constexpr int NW = kDqThreads / 64;         // waves
+    constexpr int KT = BN * ROWB;               // one tensor's key tile in LDS
+    constexpr int BUF = 2 * KT;                 // K tile, then V tile
+    constexpr int NBW = KT / 1024 / NW;         // 1-KB direct loads per wave, tensor and tile
+    static_assert(NBW >= 1 && NBW * NW * 1024 == KT, "key tile must split over the waves");
+    static_assert(BM == NW * 32, "32 query rows per wave");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * BUF];
+    lds_u8* const L = (lds_u8*)smem;
+    const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(L));
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31, hw = lane >> 5;
     const int total = a.q_tiles * a.B * a.H;
     const int id = xcd_logical_id(blockIdx.x, total);
@@ -266,51 +239,110 @@ __global__ __launch_bounds__(kDqThreads) void bwd_dq_kernel(const BwdArgs a) {
     const float lse2 = lse[qr] * 1.4426950408889634f;
     const float dlt = dl[qr];
     const float c = a.scale_log2;
+    // the Q/dO loads land before any direct load is issued
+    wait_lds_dma();
 
-    const TileOffsets<D> off(lane);
+    // key tile j of the sequence: first key k0 and end ke of its range
+    const Ranges rg = key_ranges(a, chunk);
+    const int n0 = (rg.e0 - rg.b0 + BN - 1) / BN;
+    const int nt = n0 + (rg.n == 2 ? (rg.e1 - rg.b1 + BN - 1) / BN : 0);
+    auto tile_at = [&](int j, int& k0, int& ke) __attribute__((always_inline)) {
+        if (j < n0) {
+            k0 = rg.b0 + j * BN;
+            ke = rg.e0;
+        } else {
+            k0 = rg.b1 + (j - n0) * BN;
+            ke = rg.e1;
+        }
+    };
+    // Direct loads of key tile j into buffer u (rows past ke repeat row
+    // ke - 1: finite values, masked below), swizzled as in the dK/dV kernel.
+    auto issue = [&](int j, int u) __attribute__((always_inline)) {
+        int k0, ke;
+        tile_at(j, k0, ke);
+        const int last = ke - 1 - k0;
+        const void* ks = uniform_ptr(kg + k0 * st);
+        const void* vs = uniform_ptr(vg + k0 * st);
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) {
+            const int blk = i * NW + wave;
+            const int ch = blk * 64 + lane;
+            const int row = ch / CPR;
+            const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
+            const uint32_t voff = static_cast<uint32_t>((min(row, last) * st + gc * 8) * 2);
+            const uint32_t l = lds_base + u * BUF + blk * 1024;
+            lds_dma16x2(ks, voff, l, vs, voff, l + KT);
+        }
+    };
+
+    const TileBases<D> tb(lane);
     f32x16_t acc[DB];
 #pragma unroll
     for (int d = 0; d < DB; ++d) acc[d] = f32x16_t{};
 
-    const Ranges rg = key_ranges(a, chunk);
-    for (int ri = 0; ri < rg.n; ++ri) {
-        const int kb0 = ri == 0 ? rg.b0 : rg.b1;
-        const int ke = ri == 0 ? rg.e0 : rg.e1;
-        for (int k0 = kb0; k0 < ke; k0 += BN) {
-            __syncthreads();  // the previous tile is no longer read
-            stage_rows<D, kDqThreads>(Ks, kg, st, k0, ke, BN, tid);
-            stage_rows<D, kDqThreads>(Vs, vg, st, k0, ke, BN, tid);
-            __syncthreads();
-            bf16x8_t pf[4];  // dS^T as the B operand, k-step j = 16 keys
+    // Key tile j from buffer U: S^T = K Q^T and dP^T = V dO^T per 32-key
+    // block kb (register i: key 32*kb + 8*(i/4) + 4*hw + i%4, query l32),
+    // dS^T as the B operand of dQ^T += K^T dS^T (k-step = 16 keys). Only a
+    // range's last tile can hold keys past the range (MASKED).
+    auto tile = [&](auto ucst, auto maskc, int k0, int ke) __attribute__((always_inline)) {
+        constexpr int U = decltype(ucst)::value;
+        constexpr bool MASKED = decltype(maskc)::value;
+        const lds_u8* Ks = L + U * BUF;
+        const lds_u8* Vs = Ks + KT;
+        const TileBases<D> off = tb.pinned();
+        bf16x8_t pf[4];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                f32x16_t s = f32x16_t{}, dp = f32x16_t{};
+        for (int kb = 0; kb < 2; ++kb) {
+            f32x16_t s = f32x16_t{}, dp = f32x16_t{};
 #pragma unroll
-                for (int kk = 0; kk < KK; ++kk) {
-                    const bf16x8_t kf = *(lds_bf16x8_t*)(Ks + kb * 32 * ROWB + off.row[kk]);
-                    const bf16x8_t vf = *(lds_bf16x8_t*)(Vs + kb * 32 * ROWB + off.row[kk]);
-                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
-                    dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, dof[kk], dp, 0, 0, 0);
-                }
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = k0 + 32 * kb + 8 * (i / 4) + 4 * hw + (i % 4);
-                    const float p = key < ke ? __builtin_amdgcn_exp2f(fmaf(s[i], c, -lse2)) : 0.f;
-                    const float ds = p * (dp[i] - dlt);
-                    pf[2 * kb + i / 8][i % 8] = static_cast<__bf16>(ds);
-                }
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8_t kf = *(const lds_bf16x8_t*)(Ks + kb * 32 * ROWB + off.row(kk));
+                const bf16x8_t vf = *(const lds_bf16x8_t*)(Vs + kb * 32 * ROWB + off.row(kk));
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, dof[kk], dp, 0, 0, 0);
             }
-            // dQ^T += K^T dS^T
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-#pragma unroll
-                for (int d = 0; d < DB; ++d) {
-                    const bf16x8_t kt = read_tr<D>(Ks + 16 * j * ROWB, off.tr[2 * d], off.tr[2 * d + 1]);
-                    acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, pf[j], acc[d], 0, 0, 0);
-                }
+            for (int i = 0; i < 16; ++i) {
+                float p = __builtin_amdgcn_exp2f(fmaf(s[i], c, -lse2));
+                if constexpr (MASKED) p = k0 + 32 * kb + 8 * (i / 4) + 4 * hw + (i % 4) < ke ? p : 0.f;
+                pf[2 * kb + i / 8][i % 8] = static_cast<__bf16>(p * (dp[i] - dlt));
             }
         }
+#pragma unroll
+        for (int j4 = 0; j4 < 4; ++j4) {
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+                const bf16x8_t kt = read_tr<D>(Ks + 16 * j4 * ROWB, off.tr_lo(d), off.tr_hi(d));
+                acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kt, pf[j4], acc[d], 0, 0, 0);
+            }
+        }
+    };
+    auto compute = [&](auto ucst, int j) __attribute__((always_inline)) {
+        int k0, ke;
+        tile_at(j, k0, ke);
+        if (ke - k0 >= BN) {
+            tile(ucst, std::false_type{}, k0, ke);
+        } else {
+            tile(ucst, std::true_type{}, k0, ke);
+        }
+    };
+
+    issue(0, 0);
+    wait_lds_dma();
+    __syncthreads();
+    for (int j = 0; j < nt; j += 2) {
+        // buffer 1 was last read in the previous tile, before the barrier
+        if (j + 1 < nt) issue(j + 1, 1);
+        compute(std::integral_constant<int, 0>{}, j);
+        wait_lds_dma();
+        __syncthreads();
+        if (j + 1 >= nt) break;
+        if (j + 2 < nt) issue(j + 2, 0);
+        compute(std::integral_constant<int, 1>{}, j + 1);
+        wait_lds_dma();
+        __syncthreads();
     }
+
     if (row_ok) {
         __bf16* dq = static_cast<__bf16*>(a.dq) + base + qrow * st;
         const float sc = a.scale;
