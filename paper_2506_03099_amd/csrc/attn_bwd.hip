@@ -508,7 +508,8 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
             const bf16x8_t vb = *(const lds_bf16x8_t*)(Vw + off.row(kk));
             dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
         }
-        const int rows = qend - q0;
+        // P and dS, 4 consecutive queries at a time (their lse, +inf for rows
+        // past qend so that P = 0, and delta)
         bf16x8_t pf[2], sf[2];
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
@@ -518,7 +519,7 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int i = 4 * g4 + e;
-                const float ml = q4 + e < rows ? x[e] * 1.4426950408889634f : __builtin_inff();
+                const float ml = x[e] * 1.4426950408889634f;
                 const float p = __builtin_amdgcn_exp2f(fmaf(s[i], c, -ml));
                 pf[i / 8][i % 8] = static_cast<__bf16>(p);
                 sf[i / 8][i % 8] = static_cast<__bf16>(p * (dp[i] - y[e]));
@@ -536,6 +537,16 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
         }
     };
 
+    // The last stage can hold rows past qend (their loads repeat row
+    // qend - 1): once its loads have landed, their lse becomes +inf, so that
+    // their P and dS are exactly zero and no stage needs a per-row mask.
+    auto seal = [&](int u, int q0) __attribute__((always_inline)) {
+        const int rows = qend - q0;
+        if (rows < BQ) {
+            if (tid >= rows && tid < BQ) ((lds_f32*)(L + VEC + u * 256))[tid] = __builtin_inff();
+            __syncthreads();
+        }
+    };
     const int n_st = (qend - qbeg + BQ - 1) / BQ;
     issue(qbeg, 0);
     wait_lds_dma();
@@ -543,11 +554,13 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
     for (int ts = 0; ts < n_st; ts += 2) {
         const int q0 = qbeg + ts * BQ;
         if (ts + 1 < n_st) issue(q0 + BQ, 1);
+        seal(0, q0);
         if (busy) compute(std::integral_constant<int, 0>{}, q0);
         wait_lds_dma();
         __syncthreads();
         if (ts + 1 >= n_st) break;
         if (ts + 2 < n_st) issue(q0 + 2 * BQ, 0);
+        seal(1, q0 + BQ);
         if (busy) compute(std::integral_constant<int, 1>{}, q0 + BQ);
         wait_lds_dma();
         __syncthreads();
