@@ -378,6 +378,7 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
     constexpr int TILE = BQ * ROWB;             // one tensor's stage tile in LDS
     constexpr int STAGE = 2 * TILE;             // Q tile, then dO tile
     constexpr int NB = TILE / 1024;             // 1-KB direct loads per tensor and stage
+    static_assert(NB % NW == 0, "stage tile must split over the waves");
     constexpr int VEC = 2 * STAGE;              // lse and delta: 2 buffers x 64 floats each
     constexpr int VT = VEC + 4 * 256;           // V rows of the workgroup's keys
     static_assert(kBwdKTile == NW * 32, "32 keys per wave");
@@ -432,7 +433,9 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
         const int last = qend - 1 - q0;
         const void* qs = uniform_ptr(qg + q0 * st);
         const void* ds = uniform_ptr(dog + q0 * st);
-        for (int blk = wave; blk < NB; blk += NW) {
+#pragma unroll
+        for (int i = 0; i < NB / NW; ++i) {
+            const int blk = i * NW + wave;
             const int ch = blk * 64 + lane;
             const int row = ch / CPR;
             const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
@@ -496,16 +499,14 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
         const lds_f32* ls = (const lds_f32*)(L + VEC + U * 256);
         const lds_f32* dls = (const lds_f32*)(L + VEC + 512 + U * 256);
         const TileBases<D> off = tb.pinned();
+        // the two chains interleaved: one's MFMA covers the other's LDS reads
         f32x16_t s = f32x16_t{}, dp = f32x16_t{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const bf16x8_t qa = *(const lds_bf16x8_t*)(Qb + off.row(kk));
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[kk], s, 0, 0, 0);
-        }
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
             const bf16x8_t da = *(const lds_bf16x8_t*)(Db + off.row(kk));
             const bf16x8_t vb = *(const lds_bf16x8_t*)(Vw + off.row(kk));
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[kk], s, 0, 0, 0);
             dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
         }
         // P and dS, 4 consecutive queries at a time (their lse, +inf for rows
