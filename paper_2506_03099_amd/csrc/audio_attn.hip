@@ -54,9 +54,10 @@ typedef __attribute__((address_space(3))) uint32_t lds_u32;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 
-// Workgroup barrier for LDS traffic only: this wave's LDS operations are
-// complete, global memory operations may still be in flight (a full
-// __syncthreads would also wait for every outstanding global load and store).
+// Workgroup barrier for LDS traffic: on gfx950 __syncthreads is
+// s_waitcnt lgkmcnt(0) + s_barrier (its workgroup-scope fence needs no
+// vector-memory wait), so this wave's LDS operations are complete while its
+// global loads and stores may still be in flight.
 __device__ __forceinline__ void lds_barrier() { __syncthreads(); }
 
 template <int D>
