@@ -208,10 +208,23 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(const BwdArgs a) 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31, hw = lane >> 5;
-    const int total = a.q_tiles * a.B * a.H;
-    const int id = xcd_logical_id(blockIdx.x, total);
-    const int t = id % a.q_tiles;
-    const int bh = id / a.q_tiles;
+    // The chunks' query tiles (which see c_0 and W + 1 chunks of keys) first,
+    // grouped per XCD so that a head's tiles share an L2; c_0's tiles (which
+    // see c_0 only) last, in plain dispatch order, so that they spread over
+    // the XCDs and fill the end of the grid.
+    const int BH = a.B * a.H;
+    const int rest = a.q_tiles - a.q_ref_tiles;
+    const int n_chunk = rest * BH;
+    int bh, t;
+    if (static_cast<int>(blockIdx.x) < n_chunk) {
+        const int id = xcd_logical_id(blockIdx.x, n_chunk);
+        bh = id / rest;
+        t = a.q_ref_tiles + id % rest;
+    } else {
+        const int r = blockIdx.x - n_chunk;
+        bh = r / a.q_ref_tiles;
+        t = r % a.q_ref_tiles;
+    }
     const int h = bh % a.H, b = bh / a.H;
     int chunk, q0, q1;
     tile_rows(a, t, BM, a.q_ref_tiles, a.q_chunk_tiles, chunk, q0, q1);
@@ -389,18 +402,22 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31, hw = lane >> 5;
-    // c_0's key tiles (every query sees them) of all heads first
+    // c_0's key tiles (every query sees them: 3.5x the work of a chunk's
+    // tile at W = 1) of all heads first, in plain dispatch order so that they
+    // spread over the 8 XCDs (grouping them per XCD would leave one XCD with
+    // all of them); the chunks' tiles after them, grouped per XCD so that a
+    // head's tiles share an L2.
     const int BH = a.B * a.H;
-    const int total = a.k_tiles * BH;
-    const int id = xcd_logical_id(blockIdx.x, total);
+    const int n_ref = a.k_ref_tiles * BH;
     int bh, t;
-    if (id < a.k_ref_tiles * BH) {
-        bh = id / a.k_ref_tiles;
-        t = id % a.k_ref_tiles;
+    if (static_cast<int>(blockIdx.x) < n_ref) {
+        bh = blockIdx.x / a.k_ref_tiles;
+        t = blockIdx.x % a.k_ref_tiles;
     } else {
         const int rest = a.k_tiles - a.k_ref_tiles;
-        bh = (id - a.k_ref_tiles * BH) / rest;
-        t = a.k_ref_tiles + (id - a.k_ref_tiles * BH) % rest;
+        const int id = xcd_logical_id(blockIdx.x - n_ref, rest * BH);
+        bh = id / rest;
+        t = a.k_ref_tiles + id % rest;
     }
     const int h = bh % a.H, b = bh / a.H;
     int chunk, k0, k1;
