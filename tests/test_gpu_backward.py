@@ -79,12 +79,22 @@ def _assert_grad(got, want, mag, what):
     (40, 2, 3, 2, 11, 128),   # three-frame c_0, W = 2
     (20, 3, 1, 0, 7, 128),    # W = 0: each chunk sees c_0 and itself
     (130, 3, 1, 1, 7, 128),   # chunks of 390 rows: 4 query tiles (last 6 rows), 2 key tiles
+    (40, 2, 3, 1, 3, 128),    # the reference chunk alone: only c_0 tiles in both grids
+    (16, 2, 1, 1, 2, 128),    # c_0 and one frame of a two-frame chunk
 ])
 def test_backward_matches_oracle(tm, T, C, R, W, frames, D):
     say(f"backward vs oracle: T={T} C={C} R={R} W={W} frames={frames} D={D}")
     got, want, mags = _run(tm, 7 * T + W, 2, 2, D, T, C, R, W, frames)
     for name, g_, w_, m_ in zip(("dq", "dk", "dv"), got, want, mags):
         _assert_grad(g_, w_, m_, f"{name} T={T} W={W} D={D}")
+
+
+def test_backward_many_heads(tm):
+    # 2 x 7 = 14 (batch, head) pairs: the grids' per-XCD grouping spans several heads
+    say("backward: B=2 H=7, T=48 C=2 R=1 W=1, 7 frames")
+    got, want, mags = _run(tm, 5, 2, 7, 64, 48, 2, 1, 1, 7)
+    for name, g_, w_, m_ in zip(("dq", "dk", "dv"), got, want, mags):
+        _assert_grad(g_, w_, m_, f"{name} B=2 H=7")
 
 
 def test_backward_21_frame_sequence(tm):
