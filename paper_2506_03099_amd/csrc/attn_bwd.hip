@@ -381,8 +381,9 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(const BwdArgs a) 
 // dP = dO V^T) sit in LDS. The 32-query stages of Q, dO, lse and delta arrive
 // by direct global->LDS loads into two alternating buffers, the next stage's
 // loads in flight during the current stage's arithmetic; one barrier per
-// stage. Two workgroups per CU keep the SIMDs' two waves out of step, so one
-// wave's softmax arithmetic overlaps the other's MFMAs.
+// stage. Two workgroups per CU keep the SIMDs' two waves out of step, so that
+// one wave's softmax arithmetic can overlap the other's MFMAs (partly: two
+// waves that both alternate the two kinds of work overlap only in part).
 template <int D>
 __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs a) {
     constexpr int ROWB = D * 2, KK = D / 16, DB = D / 32, CPR = D / 8;
@@ -443,7 +444,8 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
     const float* dl = a.delta + (static_cast<int64_t>(b) * a.H + h) * a.L;
 
     // Direct loads of the stage starting at query q0 into buffer u: rows past
-    // qend repeat row qend - 1 (finite values, masked below). Each 1-KB block
+    // qend repeat row qend - 1 (finite values; seal() below zeroes their P
+    // and dS). Each 1-KB block
     // holds 64 consecutive 16-byte LDS chunks of the swizzled tile; the lane
     // whose chunk is logical chunk gc of row `row` fetches that chunk.
     auto issue = [&](int q0, int u) __attribute__((always_inline)) {
