@@ -91,7 +91,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the hot path here is the single-GPU kernel "
-              f"(it would shard by head across GPUs, which this build does not do); "
+              f"(it would shard by head across GPUs; no multi-GPU path is implemented); "
               f"--gpus {args.gpus} is not supported.", file=sys.stderr)
         sys.exit(2)
 
