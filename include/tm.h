@@ -177,6 +177,20 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
                                     const tm_kv_cache* cache, const void* k, const void* v,
                                     int32_t n_frames, void* o, float* lse, hipStream_t stream);
 
+/* The same attention, with the output stored as fp32 instead of the
+ * descriptor's dtype (paper Sec. 4.2, the attention equation; for callers
+ * that keep the attention output in fp32, e.g. to add it to an fp32 residual
+ * stream). Arguments, checks and launch are those of
+ * tm_sparse_causal_attn_fwd, except o: device fp32 [B, Lq, H, D], 16-byte
+ * aligned. For TM_BF16 inputs the arithmetic is the same kernel's, and only
+ * the final rounding of O/l to bf16 (nearest even) is left out, so rounding o
+ * to bf16 gives the bf16 call's output bit for bit; o then must not overlap q
+ * at all. For TM_F32 inputs this is tm_sparse_causal_attn_fwd (o may be q). */
+tm_status tm_sparse_causal_attn_fwd_f32out(const tm_attn_desc* desc, const void* q,
+                                           int32_t q_chunk, const tm_kv_cache* cache,
+                                           const void* k, const void* v, int32_t n_frames,
+                                           float* o, float* lse, hipStream_t stream);
+
 /* Backward pass of the full-sequence form (training the student through the
  * attention of Sec. 4.2): given dO = dL/dO, the gradients
  *   dV = P^T dO, dS = P * (dO V^T - rowsum(dO * O)), dQ = scale dS K,
@@ -242,6 +256,18 @@ typedef struct tm_audio_desc {
 tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* desc, const void* q, int32_t first_frame,
                                   int32_t n_tok, const void* ak, const void* av,
                                   const int32_t* face, void* o, hipStream_t stream);
+
+/* The same audio cross-attention with the output stored as fp32 (paper
+ * Sec. 4.1; for callers that keep the cross-attention output in fp32):
+ * arguments and checks as tm_audio_cross_attn_fwd, except o: device fp32
+ * [B, n_tok, H, D], 16-byte aligned, not overlapping q. The arithmetic is the
+ * bf16 call's; only the final rounding to bf16 (nearest even) is left out,
+ * so rounding o to bf16 gives that call's output bit for bit. Rows without a
+ * face get zeros. */
+tm_status tm_audio_cross_attn_fwd_f32out(const tm_audio_desc* desc, const void* q,
+                                         int32_t first_frame, int32_t n_tok, const void* ak,
+                                         const void* av, const int32_t* face, float* o,
+                                         hipStream_t stream);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* tm_last_error(void);

@@ -20,7 +20,9 @@ What it computes, and where the paper defines it:
   form and in the streaming form that keeps every appended chunk's K/V on the
   host (Sec. 4.3, "KV & Embedding Cachings").
 * ``brute``     -- an independent fp64 per-query enumeration of the same key
-  set, used to pin ``attention`` on tiny inputs.
+  set, used to pin ``attention`` on tiny inputs, and an fp64 per-element
+  loop of the gradients and of their absolute-product sums, used to pin
+  ``backward``.
 * ``producer``  -- the RMS normalisation of query and key rows that precedes
   the attention and the KV cache (the fused K/V producer).
 * ``backward``  -- the gradients dQ, dK, dV of the sparse causal attention
@@ -47,7 +49,11 @@ from .attention import (  # noqa: F401
     full_sequence_attention,
     StreamHistory,
 )
-from .brute import brute_force_attention  # noqa: F401
+from .brute import brute_force_attention, brute_force_backward  # noqa: F401
 from .producer import rms_normalise  # noqa: F401
 from .audio import audio_cross_attention, audio_window  # noqa: F401
-from .backward import masked_attention_backward, full_sequence_attention_backward  # noqa: F401
+from .backward import (  # noqa: F401
+    masked_attention_backward,
+    full_sequence_attention_backward,
+    sampled_sequence_attention_backward,
+)

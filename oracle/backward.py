@@ -81,3 +81,76 @@ def full_sequence_attention_backward(q, k, v, do, g: ChunkGeometry, *, scale=Non
     if magnitudes:
         return tuple(out[:3]), tuple(out[3:])
     return tuple(out)
+
+
+def sampled_sequence_attention_backward(q, k, v, do, g: ChunkGeometry, *, q_rows, k_rows,
+                                        heads=None, scale=None, row_block: int = 1024,
+                                        dtype=np.float64):
+    """Selected gradient rows of the whole-sequence backward, for sequences
+    whose L x L matrices do not fit in memory.
+
+    The same chain rule as ``masked_attention_backward``, evaluated in blocks
+    of ``row_block`` query rows; every query row is always a complete masked
+    row over all L keys. Two passes per (batch, head):
+
+    1. for every query row i: P_i (masked row softmax of scale q_i K^T),
+       dP_i = dO_i V^T and g_i = sum_j P_ij dP_ij, kept as lse_i =
+       log sum_j exp(scale q_i.k_j) and g_i;
+    2. dQ_i = scale dS_i K for i in ``q_rows``, with dS_i = P_i * (dP_i - g_i);
+       dK_j = scale sum_i dS_ij q_i and dV_j = sum_i P_ij dO_i for j in
+       ``k_rows``, summing over every query row (P_ij = exp(s_ij - lse_i),
+       the row softmax written with its normaliser).
+
+    Returns ((dq, dk, dv), (mq, mk, mv)): dq and mq [B, len(q_rows), n_heads,
+    D], the others [B, len(k_rows), n_heads, D]; the m's are the sums of
+    absolute products as in ``masked_attention_backward``.
+    """
+    B, L, H, D = q.shape
+    if scale is None:
+        scale = 1.0 / float(np.sqrt(D))
+    sc = dtype(scale)
+    heads = list(range(H)) if heads is None else list(heads)
+    q_rows = np.asarray(q_rows, dtype=np.int64)
+    k_rows = np.asarray(k_rows, dtype=np.int64)
+    pos = np.arange(L)
+    nh = len(heads)
+    dq = np.zeros((B, len(q_rows), nh, D), dtype=dtype)
+    mq = np.zeros_like(dq)
+    dk = np.zeros((B, len(k_rows), nh, D), dtype=dtype)
+    mk, dv, mv = np.zeros_like(dk), np.zeros_like(dk), np.zeros_like(dk)
+    for b in range(B):
+        for hi, h in enumerate(heads):
+            qh, kh, vh, doh = (np.ascontiguousarray(x[b, :, h, :], dtype=dtype) for x in (q, k, v, do))
+            lse = np.empty(L, dtype=dtype)
+            gsum = np.empty(L, dtype=dtype)
+            for r0 in range(0, L, row_block):
+                rows = pos[r0:r0 + row_block]
+                mask = allowed_mask(rows, pos, g)
+                s = np.where(mask, (qh[rows] @ kh.T) * sc, -np.inf)
+                m = s.max(axis=1, keepdims=True)
+                e = np.where(mask, np.exp(s - m), dtype(0))
+                z = e.sum(axis=1, keepdims=True)
+                p = e / z
+                dp = doh[rows] @ vh.T
+                lse[rows] = m[:, 0] + np.log(z[:, 0])
+                gsum[rows] = (p * dp).sum(axis=1)
+            # dQ of the selected query rows
+            mask = allowed_mask(q_rows, pos, g)
+            s = np.where(mask, (qh[q_rows] @ kh.T) * sc, -np.inf)
+            p = np.where(mask, np.exp(s - lse[q_rows, None]), dtype(0))
+            ds = p * (doh[q_rows] @ vh.T - gsum[q_rows, None])
+            dq[b, :, hi] = sc * (ds @ kh)
+            mq[b, :, hi] = sc * (np.abs(ds) @ np.abs(kh))
+            # dK, dV of the selected keys, summed over every query row
+            ks, vs = kh[k_rows], vh[k_rows]
+            for r0 in range(0, L, row_block):
+                rows = pos[r0:r0 + row_block]
+                mask = allowed_mask(rows, k_rows, g)
+                s = np.where(mask, (qh[rows] @ ks.T) * sc, -np.inf)
+                p = np.where(mask, np.exp(s - lse[rows, None]), dtype(0))
+                ds = p * (doh[rows] @ vs.T - gsum[rows, None])
+                dk[b, :, hi] += sc * (ds.T @ qh[rows])
+                mk[b, :, hi] += sc * (np.abs(ds).T @ np.abs(qh[rows]))
+                dv[b, :, hi] += p.T @ doh[rows]
+                mv[b, :, hi] += p.T @ np.abs(doh[rows])
+    return (dq, dk, dv), (mq, mk, mv)

@@ -72,3 +72,64 @@ def brute_force_attention(q, k, v, *, T: int, C: int, R: int, W: int, scale=None
             o[i, d] = math.fsum(w[n] * v[j, d] for n, j in enumerate(keys)) / z
         lse[i] = mx + math.log(z)
     return o, lse, key_sets
+
+
+def brute_force_backward(q, k, v, do, *, T: int, C: int, R: int, W: int, scale=None):
+    """Gradients of the loss sum(O * dO) of one head, one element at a time in
+    fp64 (``math.exp``, ``math.fsum``), with the key sets enumerated as above.
+
+    Written independently of ``backward``: for each query i with key set K_i,
+        s_ij = scale q_i.k_j,  p_ij = exp(s_ij - max) / sum,
+        dp_ij = dO_i.v_j,      g_i = sum_j p_ij dp_ij,
+        ds_ij = p_ij (dp_ij - g_i)            (row Jacobian of the softmax),
+    and the three gradients, each with the sum of the absolute values of the
+    products it adds up (the bound on its rounding error when every factor
+    carries a relative error):
+        dQ_id = scale sum_j ds_ij k_jd        |  scale sum_j |ds_ij| |k_jd|
+        dK_jd = scale sum_i ds_ij q_id        |  scale sum_i |ds_ij| |q_id|
+        dV_jd = sum_i p_ij dO_id              |  sum_i p_ij |dO_id|
+    (TalkingMachines, Sec. 4.2: the attention equation over {c_0, c_{a-W}, ..,
+    c_a}, differentiated for training the student through it.)
+
+    q, k, v, do: [L, D] at positions 0..L-1. Returns ((dq, dk, dv), (mq, mk, mv)),
+    all [L, D] fp64.
+    """
+    q, k, v, do = (np.asarray(x, dtype=np.float64) for x in (q, k, v, do))
+    L, D = q.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    chunks = chunk_token_lists(L, T, C, R)
+    chunk_of = {p: ci for ci, toks in enumerate(chunks) for p in toks}
+    dq, mq = np.zeros((L, D)), np.zeros((L, D))
+    dk_terms = [[[] for _ in range(D)] for _ in range(L)]
+    mk_terms = [[[] for _ in range(D)] for _ in range(L)]
+    dv_terms = [[[] for _ in range(D)] for _ in range(L)]
+    mv_terms = [[[] for _ in range(D)] for _ in range(L)]
+    for i in range(L):
+        a = chunk_of[i]
+        keys = set()
+        for ci in {0} | set(range(max(0, a - W), a + 1)):
+            keys.update(chunks[ci])
+        keys = sorted(keys)
+        logits = [scale * math.fsum(q[i, d] * k[j, d] for d in range(D)) for j in keys]
+        mx = max(logits)
+        w = [math.exp(x - mx) for x in logits]
+        z = math.fsum(w)
+        p = [x / z for x in w]
+        dp = [math.fsum(do[i, d] * v[j, d] for d in range(D)) for j in keys]
+        gi = math.fsum(pn * dpn for pn, dpn in zip(p, dp))
+        ds = [pn * (dpn - gi) for pn, dpn in zip(p, dp)]
+        for d in range(D):
+            dq[i, d] = scale * math.fsum(ds[n] * k[j, d] for n, j in enumerate(keys))
+            mq[i, d] = scale * math.fsum(abs(ds[n]) * abs(k[j, d]) for n, j in enumerate(keys))
+        for n, j in enumerate(keys):
+            for d in range(D):
+                dk_terms[j][d].append(ds[n] * q[i, d])
+                mk_terms[j][d].append(abs(ds[n]) * abs(q[i, d]))
+                dv_terms[j][d].append(p[n] * do[i, d])
+                mv_terms[j][d].append(p[n] * abs(do[i, d]))
+    dk = np.array([[scale * math.fsum(t) for t in row] for row in dk_terms])
+    mk = np.array([[scale * math.fsum(t) for t in row] for row in mk_terms])
+    dv = np.array([[math.fsum(t) for t in row] for row in dv_terms])
+    mv = np.array([[math.fsum(t) for t in row] for row in mv_terms])
+    return (dq, dk, dv), (mq, mk, mv)

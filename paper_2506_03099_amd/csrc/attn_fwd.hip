@@ -176,7 +176,7 @@ __device__ __forceinline__ int vt_swizzle(int d) { return (d >> 1) & 7; }
 
 
 
-template <int D, bool VT>
+template <int D, bool VT, bool OF32>
 __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const AttnArgs a) {
     constexpr int BM = kTileRowsBf16;  // query rows per workgroup
     constexpr int BN = 64;             // keys per tile
@@ -577,19 +577,29 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     }
     wait_lds_dma();  // no load may still be writing LDS when the workgroup ends
 
-    // ---- epilogue: normalise, round to bf16, store rows inside the tile
+    // ---- epilogue: normalise, store rows inside the tile, rounded to bf16
+    // (nearest even) or, with OF32, as the fp32 values that rounding would take
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     const float inv = 1.f / l_tot;
     if (row_ok) {
-        __bf16* op = static_cast<__bf16*>(a.o) + bat * a.o_sb + head * a.o_sh + qrow * a.o_st;
+        const int64_t orow = bat * a.o_sb + head * a.o_sh + qrow * a.o_st;
 #pragma unroll
         for (int d = 0; d < DB; ++d) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                bf16x4_t w;
+                if constexpr (OF32) {
+                    float4 w;
+                    w.x = acc[d][4 * g + 0] * inv;
+                    w.y = acc[d][4 * g + 1] * inv;
+                    w.z = acc[d][4 * g + 2] * inv;
+                    w.w = acc[d][4 * g + 3] * inv;
+                    *reinterpret_cast<float4*>(static_cast<float*>(a.o) + orow + 32 * d + 8 * g + 4 * hw) = w;
+                } else {
+                    bf16x4_t w;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[d][4 * g + e] * inv);
-                *reinterpret_cast<bf16x4_t*>(op + 32 * d + 8 * g + 4 * hw) = w;
+                    for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[d][4 * g + e] * inv);
+                    *reinterpret_cast<bf16x4_t*>(static_cast<__bf16*>(a.o) + orow + 32 * d + 8 * g + 4 * hw) = w;
+                }
             }
         }
         if (a.lse != nullptr && hw == 0) {
@@ -701,16 +711,22 @@ __global__ __launch_bounds__(256) void attn_fwd_f32_kernel(const AttnArgs a) {
     }
 }
 
+template <int D, bool VT>
+void launch_bf16_out(const AttnArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+    if (a.o_f32) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, VT, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, VT, false>), grid, block, 0, s, a);
+}
+
 }  // namespace
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
     const dim3 grid(a.n_qtiles * a.B * a.H), block(kBf16Threads);
     if (head_dim == 128) {
-        if (a.v_blocked) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false>), grid, block, 0, s, a);
+        if (a.v_blocked) launch_bf16_out<128, true>(a, grid, block, s);
+        else launch_bf16_out<128, false>(a, grid, block, s);
     } else if (head_dim == 64) {
-        if (a.v_blocked) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false>), grid, block, 0, s, a);
+        if (a.v_blocked) launch_bf16_out<64, true>(a, grid, block, s);
+        else launch_bf16_out<64, false>(a, grid, block, s);
     } else {
         return hipErrorInvalidValue;
     }

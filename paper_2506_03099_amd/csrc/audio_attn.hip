@@ -60,7 +60,7 @@ typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 // global loads and stores may still be in flight.
 __device__ __forceinline__ void lds_barrier() { __syncthreads(); }
 
-template <int D>
+template <int D, bool OF32>
 __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const AudioArgs a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     constexpr int ROWB = D * 2;   // bytes of a K or V row
@@ -101,7 +101,10 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
 
     const int64_t st = static_cast<int64_t>(a.H) * D;  // elements per token row
     const __bf16* qb = static_cast<const __bf16*>(a.q) + static_cast<int64_t>(b) * a.n * st + h * D;
-    __bf16* ob = static_cast<__bf16*>(a.o) + static_cast<int64_t>(b) * a.n * st + h * D;
+    // output rows: bf16, or fp32 with OF32 (the same values before rounding)
+    constexpr int OES = OF32 ? 4 : 2;   // bytes per output element
+    constexpr int OCPR = D * OES / 16;  // 16-byte chunks per output row
+    unsigned char* ob = static_cast<unsigned char*>(a.o) + (static_cast<int64_t>(b) * a.n * st + h * D) * OES;
     const int32_t* fb = a.face + static_cast<int64_t>(b) * a.n;
 
     constexpr int FID = (32 * kAudioBlocksPerPart + kAudioThreads - 1) / kAudioThreads;  // per thread
@@ -181,10 +184,10 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
     for (int w = 0; w < kAudioWaves; ++w) streams |= used_l[w];
 
     // ---- zeros for the rows without a face
-    for (int i = tid; i < n_rows * CPR; i += kAudioThreads) {
-        const int ri = i / CPR;
+    for (int i = tid; i < n_rows * OCPR; i += kAudioThreads) {
+        const int ri = i / OCPR;
         if (static_cast<int>(face_l[ri]) == -1)
-            *reinterpret_cast<u32x4_t*>(ob + part_row(ri) * st + (i % CPR) * 8) = u32x4_t{0, 0, 0, 0};
+            *reinterpret_cast<u32x4_t*>(ob + (part_row(ri) * st) * OES + (i % OCPR) * 16) = u32x4_t{0, 0, 0, 0};
     }
     const float c = a.scale_log2;
     const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
@@ -314,15 +317,25 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
                                                               false, false);
             const float inv = 1.f / (__uint_as_float(lsw[0]) + __uint_as_float(lsw[1]));  // both half-waves
             if (act) {
-                __bf16* op = ob + row * st;
+                unsigned char* op = ob + (row * st) * OES;
 #pragma unroll
                 for (int d = 0; d < DB; ++d) {
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        bf16x4_t w;
+                        const int e0 = 32 * d + 8 * g + 4 * hw;  // first of the lane's 4 dimensions
+                        if constexpr (OF32) {
+                            float4 w;
+                            w.x = acc[d][4 * g + 0] * inv;
+                            w.y = acc[d][4 * g + 1] * inv;
+                            w.z = acc[d][4 * g + 2] * inv;
+                            w.w = acc[d][4 * g + 3] * inv;
+                            *reinterpret_cast<float4*>(op + e0 * 4) = w;
+                        } else {
+                            bf16x4_t w;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[d][4 * g + e] * inv);
-                        *reinterpret_cast<bf16x4_t*>(op + 32 * d + 8 * g + 4 * hw) = w;
+                            for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[d][4 * g + e] * inv);
+                            *reinterpret_cast<bf16x4_t*>(op + e0 * 2) = w;
+                        }
                     }
                 }
             }
@@ -350,7 +363,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
 // size, which covers every launch); concurrent first calls set the same value.
 constexpr int kMaxDevices = 64;
 
-template <int D>
+template <int D, bool OF32>
 hipError_t launch(const AudioArgs& a, unsigned grid, size_t lds, hipStream_t s) {
     static std::atomic<bool> attr_set[kMaxDevices];
     int dev = 0;
@@ -358,12 +371,12 @@ hipError_t launch(const AudioArgs& a, unsigned grid, size_t lds, hipStream_t s) 
     if (e != hipSuccess) return e;
     if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
     if (!attr_set[dev].load(std::memory_order_acquire)) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&audio_attn_bf16_kernel<D>),
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&audio_attn_bf16_kernel<D, OF32>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kAudioMaxLds));
         if (e != hipSuccess) return e;
         attr_set[dev].store(true, std::memory_order_release);
     }
-    hipLaunchKernelGGL(audio_attn_bf16_kernel<D>, dim3(grid), dim3(kAudioThreads), lds, s, a);
+    hipLaunchKernelGGL((audio_attn_bf16_kernel<D, OF32>), dim3(grid), dim3(kAudioThreads), lds, s, a);
     return hipGetLastError();
 }
 
@@ -374,8 +387,9 @@ hipError_t launch_audio_attn_bf16(const AudioArgs& a, int head_dim, hipStream_t 
     if (grid < 1 || grid > INT32_MAX) return hipErrorInvalidValue;
     const size_t lds = audio_lds_bytes(head_dim, a.max_keys_pad);
     if (lds > kAudioMaxLds) return hipErrorInvalidValue;
-    if (head_dim == 128) return launch<128>(a, static_cast<unsigned>(grid), lds, s);
-    if (head_dim == 64) return launch<64>(a, static_cast<unsigned>(grid), lds, s);
+    const unsigned g = static_cast<unsigned>(grid);
+    if (head_dim == 128) return a.o_f32 ? launch<128, true>(a, g, lds, s) : launch<128, false>(a, g, lds, s);
+    if (head_dim == 64) return a.o_f32 ? launch<64, true>(a, g, lds, s) : launch<64, false>(a, g, lds, s);
     return hipErrorInvalidValue;
 }
 

@@ -402,9 +402,16 @@ int64_t tm_allowed_pairs(const tm_attn_desc* desc, int32_t q_chunk, const tm_kv_
     return p.pairs;
 }
 
-tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int32_t q_chunk,
-                                    const tm_kv_cache* cache, const void* k, const void* v,
-                                    int32_t n_frames, void* o, float* lse, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The forward of both output types: o holds elements of the descriptor's
+// dtype, or fp32 when o_f32 is set (for bf16 inputs the values before the
+// final rounding; for fp32 inputs the same call).
+tm_status attn_fwd(const tm_attn_desc* desc, const void* q, int32_t q_chunk,
+                   const tm_kv_cache* cache, const void* k, const void* v, int32_t n_frames,
+                   void* o, bool o_f32, float* lse, hipStream_t stream) {
     Geo g;
     Plan p;
     tm_status st = make_plan(desc, q_chunk, cache, n_frames, &g, &p);
@@ -432,23 +439,26 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
         kv_bytes = size_t(g.B) * size_t(p.seq_len) * size_t(HD) * g.elem;
     }
     const size_t q_bytes = size_t(g.B) * size_t(p.Lq) * size_t(HD) * g.elem;
+    const size_t o_bytes = size_t(g.B) * size_t(p.Lq) * size_t(HD) * (o_f32 ? 4 : g.elem);
     const size_t lse_bytes = size_t(g.B) * size_t(g.H) * size_t(p.Lq) * sizeof(float);
     if ((st = check_ptr(q, q_bytes, "q")) != TM_OK) return st;
     if ((st = check_ptr(a.k, kv_bytes, cache ? "k_pool" : "k")) != TM_OK) return st;
     if ((st = check_ptr(a.v, kv_bytes, cache ? "v_pool" : "v")) != TM_OK) return st;
-    if ((st = check_ptr(o, q_bytes, "o")) != TM_OK) return st;
+    if ((st = check_ptr(o, o_bytes, "o")) != TM_OK) return st;
     if (lse != nullptr && (st = check_ptr(lse, lse_bytes, "lse", 4)) != TM_OK) return st;
-    if (overlaps(o, q_bytes, a.k, kv_bytes) || overlaps(o, q_bytes, a.v, kv_bytes))
+    if (overlaps(o, o_bytes, a.k, kv_bytes) || overlaps(o, o_bytes, a.v, kv_bytes))
         return fail(TM_E_ARG, "o overlaps k or v");
-    if (o != q && overlaps(o, q_bytes, q, q_bytes))
-        return fail(TM_E_ARG, "o partially overlaps q (only o == q is allowed)");
+    // In place (o == q) only when o and q have the same element type.
+    if ((o != q || o_bytes != q_bytes) && overlaps(o, o_bytes, q, q_bytes))
+        return fail(TM_E_ARG, "o overlaps q (only o == q with the same dtype is allowed)");
     if (lse != nullptr && (overlaps(lse, lse_bytes, a.k, kv_bytes) ||
                            overlaps(lse, lse_bytes, a.v, kv_bytes) ||
-                           overlaps(lse, lse_bytes, q, q_bytes) || overlaps(lse, lse_bytes, o, q_bytes)))
+                           overlaps(lse, lse_bytes, q, q_bytes) || overlaps(lse, lse_bytes, o, o_bytes)))
         return fail(TM_E_ARG, "lse overlaps another tensor");
 
     a.q = q;
     a.o = o;
+    a.o_f32 = o_f32 && g.dtype == TM_BF16;
     a.lse = lse;
     a.q_sb = a.o_sb = p.Lq * HD;
     a.q_st = a.o_st = HD;
@@ -490,6 +500,23 @@ tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int
                                             : tmk::launch_attn_f32(a, int(g.D), stream);
     if (e != hipSuccess) return fail(TM_E_DEVICE, "attention launch: %s", hipGetErrorString(e));
     return TM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tm_status tm_sparse_causal_attn_fwd(const tm_attn_desc* desc, const void* q, int32_t q_chunk,
+                                    const tm_kv_cache* cache, const void* k, const void* v,
+                                    int32_t n_frames, void* o, float* lse, hipStream_t stream) {
+    return attn_fwd(desc, q, q_chunk, cache, k, v, n_frames, o, false, lse, stream);
+}
+
+tm_status tm_sparse_causal_attn_fwd_f32out(const tm_attn_desc* desc, const void* q,
+                                           int32_t q_chunk, const tm_kv_cache* cache,
+                                           const void* k, const void* v, int32_t n_frames,
+                                           float* o, float* lse, hipStream_t stream) {
+    return attn_fwd(desc, q, q_chunk, cache, k, v, n_frames, o, true, lse, stream);
 }
 
 tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, const void* q,
@@ -566,9 +593,13 @@ tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, 
     return TM_OK;
 }
 
-tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t first_frame,
-                                  int32_t n_tok, const void* ak, const void* av,
-                                  const int32_t* face, void* o, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+tm_status audio_fwd(const tm_audio_desc* d, const void* q, int32_t first_frame, int32_t n_tok,
+                    const void* ak, const void* av, const int32_t* face, void* o, bool o_f32,
+                    hipStream_t stream) {
     if (d == nullptr) return fail(TM_E_ARG, "descriptor is NULL");
     if (d->dtype != TM_BF16) return fail(TM_E_DTYPE, "audio cross-attention runs in TM_BF16 only");
     if (d->batch < 1 || d->heads < 1) return fail(TM_E_SHAPE, "batch and heads must be >= 1");
@@ -606,6 +637,7 @@ tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t
 
     const size_t HD = size_t(d->heads) * size_t(d->head_dim);
     const size_t q_bytes = size_t(d->batch) * size_t(n_tok) * HD * 2;
+    const size_t o_bytes = size_t(d->batch) * size_t(n_tok) * HD * (o_f32 ? 4 : 2);
     const size_t a_bytes = size_t(d->batch) * size_t(d->streams) * size_t(La) * HD * 2;
     const size_t f_bytes = size_t(d->batch) * size_t(n_tok) * sizeof(int32_t);
     tm_status st;
@@ -613,12 +645,12 @@ tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t
     if ((st = check_ptr(ak, a_bytes, "ak")) != TM_OK) return st;
     if ((st = check_ptr(av, a_bytes, "av")) != TM_OK) return st;
     if ((st = check_ptr(face, f_bytes, "face", 4)) != TM_OK) return st;
-    if ((st = check_ptr(o, q_bytes, "o")) != TM_OK) return st;
-    if (overlaps(o, q_bytes, ak, a_bytes) || overlaps(o, q_bytes, av, a_bytes) ||
-        overlaps(o, q_bytes, face, f_bytes))
+    if ((st = check_ptr(o, o_bytes, "o")) != TM_OK) return st;
+    if (overlaps(o, o_bytes, ak, a_bytes) || overlaps(o, o_bytes, av, a_bytes) ||
+        overlaps(o, o_bytes, face, f_bytes))
         return fail(TM_E_ARG, "o overlaps ak, av or face");
-    if (o != q && overlaps(o, q_bytes, q, q_bytes))
-        return fail(TM_E_ARG, "o partially overlaps q (only o == q is allowed)");
+    if ((o != q || o_f32) && overlaps(o, o_bytes, q, q_bytes))
+        return fail(TM_E_ARG, "o overlaps q (only o == q with the same dtype is allowed)");
 
     const int64_t rows_per_frame = std::min<int64_t>(T, n_tok);
     const int64_t blocks = ceil_div(rows_per_frame, 32);
@@ -643,11 +675,29 @@ tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t
     a.n_frames = int32_t(n_frames);
     a.parts = int32_t(parts);
     a.max_keys_pad = int32_t(keys_pad);
+    a.o_f32 = o_f32 ? 1 : 0;
     const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt(float(d->head_dim));
     a.scale_log2 = float(double(scale) * 1.4426950408889634);
     const hipError_t e = tmk::launch_audio_attn_bf16(a, d->head_dim, stream);
     if (e != hipSuccess) return fail(TM_E_DEVICE, "audio attention launch: %s", hipGetErrorString(e));
     return TM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* d, const void* q, int32_t first_frame,
+                                  int32_t n_tok, const void* ak, const void* av,
+                                  const int32_t* face, void* o, hipStream_t stream) {
+    return audio_fwd(d, q, first_frame, n_tok, ak, av, face, o, false, stream);
+}
+
+tm_status tm_audio_cross_attn_fwd_f32out(const tm_audio_desc* d, const void* q,
+                                         int32_t first_frame, int32_t n_tok, const void* ak,
+                                         const void* av, const int32_t* face, float* o,
+                                         hipStream_t stream) {
+    return audio_fwd(d, q, first_frame, n_tok, ak, av, face, o, true, stream);
 }
 
 const char* tm_last_error(void) { return g_err.c_str(); }

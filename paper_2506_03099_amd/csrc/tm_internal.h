@@ -37,6 +37,7 @@ struct AttnArgs {
     int64_t k_sb, k_st, k_sh;
     int64_t v_sb, v_st, v_sh;
     int64_t o_sb, o_st, o_sh;
+    int32_t o_f32;  // bf16 kernel: store O as fp32 (the values before the final rounding)
     int32_t v_blocked;
     int32_t B, H, Lq;
     float scale_log2;  // softmax scale * log2(e)
@@ -95,6 +96,7 @@ struct AudioArgs {
     int32_t n_frames;      // latent frames the n rows span
     int32_t parts;         // workgroups per (batch, head, frame)
     int32_t max_keys_pad;  // most window keys of any frame, rounded up to 32
+    int32_t o_f32;         // store o as fp32 (the values before the final rounding)
     float scale_log2;      // softmax scale * log2(e)
 };
 

@@ -102,9 +102,13 @@ def lib() -> ctypes.CDLL:
                                               P, ctypes.c_int32, P]),
             "tm_sparse_causal_attn_fwd": (ctypes.c_int, [D, P, ctypes.c_int32, P, P, P,
                                                          ctypes.c_int32, P, P, P]),
+            "tm_sparse_causal_attn_fwd_f32out": (ctypes.c_int, [D, P, ctypes.c_int32, P, P, P,
+                                                                ctypes.c_int32, P, P, P]),
             "tm_allowed_pairs": (ctypes.c_int64, [D, ctypes.c_int32, P, ctypes.c_int32]),
             "tm_audio_cross_attn_fwd": (ctypes.c_int, [AD, P, ctypes.c_int32, ctypes.c_int32, P, P,
                                                        P, P, P]),
+            "tm_audio_cross_attn_fwd_f32out": (ctypes.c_int, [AD, P, ctypes.c_int32,
+                                                              ctypes.c_int32, P, P, P, P, P]),
             "tm_sparse_causal_attn_bwd": (ctypes.c_int, [D, ctypes.c_int32, P, P, P, P, P, P, P,
                                                          P, P, P, P]),
             "tm_last_error": (ctypes.c_char_p, []),
@@ -247,6 +251,20 @@ def tm_sparse_causal_attn_fwd(desc: tm_attn_desc, q, q_chunk: int, cache: KVCach
     return o
 
 
+def tm_sparse_causal_attn_fwd_f32out(desc: tm_attn_desc, q, q_chunk: int,
+                                     cache: KVCache | None = None, k=None, v=None,
+                                     n_frames: int = 0, o=None, lse=None, stream=None):
+    """The same attention with an fp32 output (``o`` allocated as fp32 like q
+    if not given); returns ``o``."""
+    if o is None:
+        o = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    h = cache.handle if cache is not None else None
+    _check(lib().tm_sparse_causal_attn_fwd_f32out(ctypes.byref(desc), _ptr(q), q_chunk, h, _ptr(k),
+                                                  _ptr(v), n_frames, _ptr(o), _ptr(lse),
+                                                  _stream(stream)))
+    return o
+
+
 def make_audio_desc(batch, heads, head_dim, tokens_per_frame, audio_per_frame, audio_frames,
                     streams=1, half_window=2, dtype="bf16", softmax_scale=0.0) -> tm_audio_desc:
     if isinstance(dtype, torch.dtype):
@@ -269,6 +287,19 @@ def tm_audio_cross_attn_fwd(desc: tm_audio_desc, q, first_frame: int, ak, av, fa
         o = torch.empty_like(q)
     _check(lib().tm_audio_cross_attn_fwd(ctypes.byref(desc), _ptr(q), first_frame, n_tok, _ptr(ak),
                                          _ptr(av), _ptr(face), _ptr(o), _stream(stream)))
+    return o
+
+
+def tm_audio_cross_attn_fwd_f32out(desc: tm_audio_desc, q, first_frame: int, ak, av, face,
+                                   o=None, n_tok: int | None = None, stream=None):
+    """The audio cross-attention with an fp32 output; returns ``o``."""
+    if n_tok is None:
+        n_tok = q.shape[1]
+    if o is None:
+        o = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check(lib().tm_audio_cross_attn_fwd_f32out(ctypes.byref(desc), _ptr(q), first_frame, n_tok,
+                                                _ptr(ak), _ptr(av), _ptr(face), _ptr(o),
+                                                _stream(stream)))
     return o
 
 

@@ -270,3 +270,50 @@ def draw_audio(w: AudioWorkload, *, layer: int = 0, base_seed: int = 0):
         res[name], res[name + "_bits"] = vals, bits
     res["face"] = face_ids(w.grid_h, w.grid_w, w.n_frames, w.streams, w.batch)
     return res
+
+
+# --------------------------------------------------------------------------- rising scores
+
+
+def draw_rising_sequence(wid: int, batch: int, n_tok: int, heads: int, head_dim: int, *,
+                         cold_tokens: int, gamma_lo: float, gamma_hi: float, dtype: str,
+                         base_seed: int = 0):
+    """q, k, v ``[B, n_tok, H, D]`` whose scores rise steeply along the key
+    positions: every query row is the RMS-normalised ``2 u + r`` for one random
+    unit-RMS direction ``u`` per (batch, head) and noise ``r``; the keys at
+    positions ``>= cold_tokens`` are ``gamma(p) u + r / 2`` with ``gamma``
+    growing linearly from ``gamma_lo`` to ``gamma_hi`` over those positions,
+    the first ``cold_tokens`` keys are RMS-normalised noise, values are N(0, 1).
+    With the default scale a key at position p then scores about
+    ``0.9 sqrt(D) gamma(p)`` against every query (log-e units), far above the
+    first keys' scores. Returns the same dict as ``draw_qkv_sequence``.
+    """
+    res = {}
+    per = {"q": [], "k": [], "v": []}
+    for b in range(batch):
+        rng = _rng(wid, b, FULL_SEQUENCE_CHUNK, 0, 0, 9, base_seed)
+        u = rng.standard_normal((1, heads, head_dim), dtype=np.float32)
+        u /= np.sqrt(np.mean(u * u, axis=-1, keepdims=True))
+        q = 2.0 * u + rng.standard_normal((n_tok, heads, head_dim), dtype=np.float32)
+        q /= np.sqrt(np.mean(q * q, axis=-1, keepdims=True))
+        k = rng.standard_normal((n_tok, heads, head_dim), dtype=np.float32)
+        k /= np.sqrt(np.mean(k * k, axis=-1, keepdims=True))
+        hot = np.arange(n_tok) >= cold_tokens
+        n_hot = int(hot.sum())
+        if n_hot:
+            gam = np.linspace(gamma_lo, gamma_hi, n_hot, dtype=np.float32)[:, None, None]
+            k[hot] = gam * u + 0.5 * k[hot]
+        v = rng.standard_normal((n_tok, heads, head_dim), dtype=np.float32)
+        per["q"].append(q)
+        per["k"].append(k)
+        per["v"].append(v)
+    for name, xs in per.items():
+        x = np.stack(xs).astype(np.float32)
+        if dtype == "bf16":
+            bits = f32_to_bf16_bits(x)
+            res[name], res[name + "_bits"] = bf16_bits_to_f32(bits), bits
+        elif dtype == "f32":
+            res[name] = x
+        else:
+            raise ValueError(f"unknown dtype {dtype!r}")
+    return res

@@ -128,3 +128,63 @@ def test_backward_is_deterministic_and_checks_arguments(tm):
     with pytest.raises(tm.TMError) as e:  # too few rows for the frames asked
         tm.tm_sparse_causal_attn_bwd(desc, frames + 1, q, k, v, o, lse, do)
     assert e.value.status == tm.TM_E_ARG
+
+
+def _chunk_tile_rows(g, L, tile, per_chunk, rng):
+    """In every chunk: its first two and last two rows, both rows at each of
+    its first three and last three tile boundaries (tiles are chunk-aligned, so
+    the last tile of a chunk is its ragged tail), and ``per_chunk`` random rows."""
+    from oracle.attention import chunk_start
+    rows = set()
+    a = 0
+    while chunk_start(a, g) < L:
+        lo, hi = chunk_start(a, g), min(chunk_start(a + 1, g), L)
+        rows.update({lo, lo + 1, hi - 2, hi - 1})
+        bounds = list(range(lo + tile, hi, tile))
+        for b in bounds[:3] + bounds[-3:]:
+            rows.update({b - 1, b})
+        rows.update(rng.choice(np.arange(lo, hi), size=per_chunk, replace=False).tolist())
+        a += 1
+    return np.array(sorted(rows))
+
+
+def test_backward_480p_full_sequence_sampled(tm):
+    """The shape the benchmark times: 21 latent frames x 1560 tokens (c_0 of one
+    frame, six chunks of 3 frames, one of 2), D = 128, two heads. Query tiles
+    of 128 rows leave tails of 24 (c_0), 72 (3-frame chunks) and 48 rows (the
+    last chunk); key tiles likewise. The oracle computes dQ for rows sampled in
+    every chunk and dK/dV for keys sampled in every chunk, each over complete
+    masked rows (``sampled_sequence_attention_backward``), head 1 of 2."""
+    from oracle.backward import sampled_sequence_attention_backward
+    from synth import draw_qkv_sequence, draw_tensor
+    from synth.inputs import FULL_SEQUENCE_CHUNK, Workload
+
+    B, H, D, T, C, R, W, frames = 1, 2, 128, 1560, 3, 1, 1, 21
+    L = frames * T
+    w = Workload(460, "bwd_480p", "bf16", B, H, D, T, C, R, W, n_frames=frames)
+    d = draw_qkv_sequence(w)
+    do, do_bits = draw_tensor((L, H, D), wid=w.wid, b=0, chunk=FULL_SEQUENCE_CHUNK, step=0,
+                              layer=0, tensor_id=3, rms_normalise=False, dtype="bf16")
+    dev = lambda bits: torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(
+        torch.bfloat16).cuda()
+    qd, kd, vd = (dev(d[n + "_bits"]) for n in "qkv")
+    dod = dev(do_bits[None])
+    desc = tm.make_desc(B, H, D, T, C, R, W, "bf16")
+    say("backward 480p: forward + backward, 21 x 1560 tokens, 2 heads")
+    lse = torch.empty(B, H, L, dtype=torch.float32, device="cuda")
+    o = tm.tm_sparse_causal_attn_fwd(desc, qd, -1, k=kd, v=vd, n_frames=frames, lse=lse)
+    dq, dk, dv = tm.tm_sparse_causal_attn_bwd(desc, frames, qd, kd, vd, o, lse, dod)
+    torch.cuda.synchronize()
+    g = ChunkGeometry(T, C, R, W)
+    rng = np.random.default_rng(21)
+    q_rows = _chunk_tile_rows(g, L, 128, 6, rng)
+    k_rows = _chunk_tile_rows(g, L, 128, 6, rng)
+    say(f"backward 480p oracle: {len(q_rows)} dQ rows, {len(k_rows)} dK/dV rows, head 1")
+    (wq, wk, wv), (mq, mk, mv) = sampled_sequence_attention_backward(
+        d["q"], d["k"], d["v"], do[None], g, q_rows=q_rows, k_rows=k_rows, heads=[1])
+    got_q = dq.float().cpu().numpy()[:, q_rows][:, :, [1]]
+    got_k = dk.float().cpu().numpy()[:, k_rows][:, :, [1]]
+    got_v = dv.float().cpu().numpy()[:, k_rows][:, :, [1]]
+    _assert_grad(got_q, wq, mq, "dq 480p")
+    _assert_grad(got_k, wk, mk, "dk 480p")
+    _assert_grad(got_v, wv, mv, "dv 480p")

@@ -152,3 +152,76 @@ def test_magnitudes_bound_the_gradients():
                                                    magnitudes=True)
     dq, dk, dv = bwd.masked_attention_backward(q[0, :, 0], k[0, :, 0], v[0, :, 0], ones, mask, 0.5)
     assert np.allclose(mdv, dv)  # dO = 1 > 0: |P|^T |dO| = P^T dO
+
+
+# --------------------------------------------------------------------------- magnitudes, pinned from both sides
+
+_MAG_CASES = ((3, 2, 1, 1, 7, 4), (2, 3, 3, 0, 9, 3), (4, 1, 1, 2, 6, 5))
+
+
+def _magnitudes_match_brute_force():
+    """The oracle's gradients and absolute-product sums against the fp64
+    element loop of ``oracle.brute`` (a second construction: key sets as
+    Python sets, per-element math.fsum)."""
+    from oracle.brute import brute_force_backward
+    for (T, C, R, W, frames, D) in _MAG_CASES:
+        g = ChunkGeometry(T, C, R, W)
+        (q, k, v, do), L = _case(T * 7 + W, g, frames, D=D)
+        (bg, bm) = brute_force_backward(q[0, :, 0], k[0, :, 0], v[0, :, 0], do[0, :, 0],
+                                        T=T, C=C, R=R, W=W)
+        grads, mags = bwd.full_sequence_attention_backward(q, k, v, do, g, magnitudes=True)
+        for mine, ref in zip(grads + mags, bg + bm):
+            if not np.allclose(mine[0, :, 0], ref, rtol=1e-12, atol=1e-14):
+                return False
+    return True
+
+
+def test_magnitudes_match_brute_force():
+    assert _magnitudes_match_brute_force()
+
+
+def _magnitude_mutant(kind):
+    real = bwd.masked_attention_backward
+
+    def f(q, k, v, do, mask, scale, *, dtype=np.float64, magnitudes=False):
+        grads = real(q, k, v, do, mask, scale, dtype=dtype)
+        if not magnitudes:
+            return grads
+        q, k, v, do = (np.asarray(x, dtype=dtype) for x in (q, k, v, do))
+        s = np.where(mask, (q @ k.T) * scale, -np.inf)
+        e = np.where(mask, np.exp(s - s.max(axis=1, keepdims=True)), 0.0)
+        p = e / e.sum(axis=1, keepdims=True)
+        dp = do @ v.T
+        ds = p * (dp - (p * dp).sum(axis=1, keepdims=True))
+        a = np.abs(dp * p) if kind == "abs_dp_for_ds" else np.abs(ds)
+        sq = 1.0 if kind == "scale_dropped" else scale
+        mq = sq * (a @ np.abs(k))
+        mk = sq * ((a @ np.abs(q)) if kind == "untransposed_dk" else (a.T @ np.abs(q)))
+        mv = (p.T @ do) if kind == "dv_no_abs" else (p.T @ np.abs(do))
+        return grads, (mq, mk, mv)
+    return f
+
+
+@pytest.mark.parametrize("kind", ["scale_dropped", "abs_dp_for_ds", "untransposed_dk", "dv_no_abs"])
+def test_magnitude_mutants_fail_the_brute_force_pin(monkeypatch, kind):
+    monkeypatch.setattr(bwd, "masked_attention_backward", _magnitude_mutant(kind))
+    assert not _magnitudes_match_brute_force()
+
+
+def test_sampled_backward_equals_the_full_oracle():
+    """Row blocks and selected rows change nothing: the sampled form equals the
+    full-matrix oracle on the rows it returns (ragged blocks of 7 rows, two
+    batch elements, a subset of heads, W = 1 and W = 2)."""
+    for (T, C, R, W, frames) in ((5, 2, 1, 1, 9), (3, 2, 3, 2, 12)):
+        g = ChunkGeometry(T, C, R, W)
+        (q, k, v, do), L = _case(31 + W, g, frames, D=6, B=2, H=3)
+        grads, mags = bwd.full_sequence_attention_backward(q, k, v, do, g, heads=[0, 2],
+                                                           magnitudes=True)
+        rng = np.random.default_rng(W)
+        qr = np.unique(np.r_[0, L - 1, rng.choice(L, 9, replace=False)])
+        kr = np.unique(np.r_[0, L - 1, rng.choice(L, 9, replace=False)])
+        sg, sm = bwd.sampled_sequence_attention_backward(q, k, v, do, g, q_rows=qr, k_rows=kr,
+                                                         heads=[0, 2], row_block=7)
+        for i, (full, part) in enumerate(zip(grads + mags, sg + sm)):
+            rows = qr if i % 3 == 0 else kr
+            assert np.allclose(full[:, rows], part, rtol=1e-12, atol=1e-14), i
