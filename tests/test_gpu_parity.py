@@ -19,8 +19,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import (assert_close, assert_rounds_to, chunk_to_dev, from_dev, sample_rows,
-                         say, to_dev)
+from gpu_helpers import (LSE_ATOL, assert_close, assert_rounds_to, chunk_to_dev, from_dev,
+                         sample_rows, say, to_dev)
 from oracle import ChunkGeometry, StreamHistory, full_sequence_attention
 from oracle.attention import chunk_start
 from synth import WORKLOADS, draw_chunk, draw_qkv_sequence
@@ -159,7 +159,7 @@ def test_full_sequence_matches_oracle_every_element(tm, case):
     o, of = _fwd(tm, desc, dtype, q, -1, k=k, v=v, n_frames=frames, lse=lse)
     o_ref, lse_ref = full_sequence_attention(d["q"], d["k"], d["v"], g)
     _check(o, of, o_ref, dtype, f"{name} o")
-    np.testing.assert_allclose(from_dev(lse), lse_ref, rtol=0, atol=1e-4 if dtype == "f32" else 2e-3)
+    np.testing.assert_allclose(from_dev(lse), lse_ref, rtol=0, atol=LSE_ATOL[dtype])
     # each chunk on its own (mode with explicit ranges)
     n_chunks = 1 + -(-(L - R * T) // (C * T)) if L > R * T else 1
     chunks = range(n_chunks) if n_chunks <= 12 else sorted({0, 1, 2, 3, n_chunks // 2, n_chunks - 2, n_chunks - 1})
@@ -212,7 +212,7 @@ def test_streaming_matches_oracle_history(tm, case):
         o_ref, lse_ref = hist.attend(dd["q"], chunk)
         _check(o, of, o_ref, dtype, f"{name} chunk {chunk} step {step}")
         np.testing.assert_allclose(from_dev(lse), lse_ref, rtol=0,
-                                   atol=1e-4 if dtype == "f32" else 2e-3)
+                                   atol=LSE_ATOL[dtype])
 
 
 def test_tiny_f32_workload_streaming_and_full_sequence(tm):
@@ -423,7 +423,7 @@ def test_480p_chunk_sampled(tm):
     o_ref, lse_ref = hist.attend(dd["q"], w.n_chunks, heads=heads, rows=rows)
     got = from_dev(o)[:, rows][:, :, heads]
     assert_close(got, o_ref, "bf16", "480p chunk")
-    np.testing.assert_allclose(from_dev(lse)[:, heads][:, :, rows], lse_ref, rtol=0, atol=2e-3)
+    np.testing.assert_allclose(from_dev(lse)[:, heads][:, :, rows], lse_ref, rtol=0, atol=LSE_ATOL["bf16"])
     # output statistics over every head and row: RMS ~ sqrt(e / 10920)
     rms = float(torch.sqrt((o.float() ** 2).mean()))
     assert abs(rms / np.sqrt(np.e / 10920) - 1) < 0.1
