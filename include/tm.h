@@ -210,6 +210,22 @@ tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, 
                                     const void* dout, float* delta, void* dq, void* dk, void* dv,
                                     hipStream_t stream);
 
+/* The same backward pass without the caller's workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * or harnesses that forbid allocation): delta lives in a device-global array
+ * of the library, 8 MiB per GPU (room for B * H * L <= 2^21 rows), which each
+ * GPU the library runs on holds until the process ends. Arguments, checks,
+ * launches and results are those of tm_sparse_causal_attn_bwd without delta;
+ * B * H * L above 2^21 returns TM_E_CAPACITY. The call allocates nothing.
+ * Every call on one GPU uses that GPU's one array (each call writes delta
+ * before reading it): calls that overlap in time on one GPU, on different
+ * streams or from different threads, race and give wrong gradients; order
+ * them. */
+tm_status tm_sparse_causal_attn_bwd_noalloc(const tm_attn_desc* desc, int32_t n_frames,
+                                            const void* q, const void* k, const void* v,
+                                            const void* o, const float* lse, const void* dout,
+                                            void* dq, void* dk, void* dv, hipStream_t stream);
+
 /* Number of allowed (query, key) pairs per (batch, head) of the call the same
  * arguments would make (4*D of FLOPs each); -1 on invalid arguments. Pure host
  * arithmetic, launches nothing; the streaming form reads the cache

@@ -32,6 +32,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "tm_device.h"
@@ -623,12 +624,43 @@ hipError_t launch_bwd(const BwdArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Workspace of the allocation-free backward entry point: delta for up to
+// kBwdScratchFloats (batch, head, token) rows, in a device-global array that
+// every GPU the library runs on holds until the process ends. Host code never
+// passes this symbol to a kernel (on the host it names a stand-in, not the
+// device copy): it uses the address hipGetSymbolAddress returns for the
+// current device.
+__device__ __align__(256) float scratch[kBwdScratchFloats];
+
+constexpr int kMaxScratchDevices = 64;
+
 }  // namespace
 
 hipError_t launch_attn_bwd_bf16(const BwdArgs& a, int head_dim, hipStream_t s) {
     if (head_dim == 128) return launch_bwd<128>(a, s);
     if (head_dim == 64) return launch_bwd<64>(a, s);
     return hipErrorInvalidValue;
+}
+
+hipError_t bwd_scratch_address(float** out) {
+    // One address per device, looked up once, with that device current
+    // (every GPU holds its own copy of the array).
+    static std::atomic<float*> addr[kMaxScratchDevices];
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    float* p = addr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        void* q = nullptr;
+        e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (q == nullptr) return hipErrorInvalidSymbol;
+        p = static_cast<float*>(q);
+        addr[dev].store(p, std::memory_order_release);  // concurrent first calls store the same value
+    }
+    *out = p;
+    return hipSuccess;
 }
 
 }  // namespace tmk

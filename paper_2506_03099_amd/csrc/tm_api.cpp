@@ -519,10 +519,16 @@ tm_status tm_sparse_causal_attn_fwd_f32out(const tm_attn_desc* desc, const void*
     return attn_fwd(desc, q, q_chunk, cache, k, v, n_frames, o, true, lse, stream);
 }
 
-tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, const void* q,
-                                    const void* k, const void* v, const void* o, const float* lse,
-                                    const void* dout, float* delta, void* dq, void* dk, void* dv,
-                                    hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The backward with a caller's delta workspace, or (delta == nullptr) with the
+// library's device-global workspace, which allocates nothing.
+tm_status attn_bwd(const tm_attn_desc* desc, int32_t n_frames, const void* q, const void* k,
+                   const void* v, const void* o, const float* lse, const void* dout, float* delta,
+                   void* dq, void* dk, void* dv, hipStream_t stream) {
+    const bool use_scratch = delta == nullptr;
     Geo g;
     tm_status st = check_desc(desc, &g);
     if (st != TM_OK) return st;
@@ -530,6 +536,12 @@ tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, 
     if (n_frames < 1) return fail(TM_E_SHAPE, "n_frames must be >= 1");
     const int64_t L = int64_t(n_frames) * g.T;
     if (L > kMaxTokens) return fail(TM_E_SHAPE, "sequence too long (more than 2^30 tokens)");
+    if (use_scratch && g.B * g.H * L > tmk::kBwdScratchFloats)
+        return fail(TM_E_CAPACITY,
+                    "batch * heads * tokens = %lld exceeds the %lld rows of the library's "
+                    "workspace; use tm_sparse_causal_attn_bwd with a caller-owned delta",
+                    static_cast<long long>(g.B * g.H * L),
+                    static_cast<long long>(tmk::kBwdScratchFloats));
     const size_t t_bytes = size_t(g.B) * size_t(L) * size_t(g.H) * size_t(g.D) * 2;
     const size_t r_bytes = size_t(g.B) * size_t(g.H) * size_t(L) * sizeof(float);
     const void* ins[] = {q, k, v, o, dout};
@@ -537,7 +549,7 @@ tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, 
     for (int i = 0; i < 5; ++i)
         if ((st = check_ptr(ins[i], t_bytes, in_names[i])) != TM_OK) return st;
     if ((st = check_ptr(lse, r_bytes, "lse", 4)) != TM_OK) return st;
-    if ((st = check_ptr(delta, r_bytes, "delta", 4)) != TM_OK) return st;
+    if (!use_scratch && (st = check_ptr(delta, r_bytes, "delta", 4)) != TM_OK) return st;
     void* outs[] = {dq, dk, dv};
     const char* out_names[] = {"dq", "dk", "dv"};
     for (int i = 0; i < 3; ++i) {
@@ -545,16 +557,23 @@ tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, 
         for (int j = 0; j < 5; ++j)
             if (overlaps(outs[i], t_bytes, ins[j], t_bytes))
                 return fail(TM_E_ARG, "%s overlaps %s", out_names[i], in_names[j]);
-        if (overlaps(outs[i], t_bytes, lse, r_bytes) || overlaps(outs[i], t_bytes, delta, r_bytes))
+        if (overlaps(outs[i], t_bytes, lse, r_bytes) ||
+            (!use_scratch && overlaps(outs[i], t_bytes, delta, r_bytes)))
             return fail(TM_E_ARG, "%s overlaps lse or delta", out_names[i]);
         for (int j = 0; j < i; ++j)
             if (overlaps(outs[i], t_bytes, outs[j], t_bytes))
                 return fail(TM_E_ARG, "%s overlaps %s", out_names[i], out_names[j]);
     }
-    for (int j = 0; j < 5; ++j)
-        if (overlaps(delta, r_bytes, ins[j], t_bytes))
-            return fail(TM_E_ARG, "delta overlaps %s", in_names[j]);
-    if (overlaps(delta, r_bytes, lse, r_bytes)) return fail(TM_E_ARG, "delta overlaps lse");
+    if (!use_scratch) {
+        for (int j = 0; j < 5; ++j)
+            if (overlaps(delta, r_bytes, ins[j], t_bytes))
+                return fail(TM_E_ARG, "delta overlaps %s", in_names[j]);
+        if (overlaps(delta, r_bytes, lse, r_bytes)) return fail(TM_E_ARG, "delta overlaps lse");
+    } else {
+        const hipError_t e = tmk::bwd_scratch_address(&delta);
+        if (e != hipSuccess)
+            return fail(TM_E_DEVICE, "workspace address: %s", hipGetErrorString(e));
+    }
 
     tmk::BwdArgs a{};
     a.q = q;
@@ -591,6 +610,25 @@ tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, 
     const hipError_t e = tmk::launch_attn_bwd_bf16(a, int(g.D), stream);
     if (e != hipSuccess) return fail(TM_E_DEVICE, "backward launch: %s", hipGetErrorString(e));
     return TM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tm_status tm_sparse_causal_attn_bwd(const tm_attn_desc* desc, int32_t n_frames, const void* q,
+                                    const void* k, const void* v, const void* o, const float* lse,
+                                    const void* dout, float* delta, void* dq, void* dk, void* dv,
+                                    hipStream_t stream) {
+    if (delta == nullptr) return fail(TM_E_ARG, "delta is NULL");
+    return attn_bwd(desc, n_frames, q, k, v, o, lse, dout, delta, dq, dk, dv, stream);
+}
+
+tm_status tm_sparse_causal_attn_bwd_noalloc(const tm_attn_desc* desc, int32_t n_frames,
+                                            const void* q, const void* k, const void* v,
+                                            const void* o, const float* lse, const void* dout,
+                                            void* dq, void* dk, void* dv, hipStream_t stream) {
+    return attn_bwd(desc, n_frames, q, k, v, o, lse, dout, nullptr, dq, dk, dv, stream);
 }
 
 }  // extern "C"

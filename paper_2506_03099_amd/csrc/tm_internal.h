@@ -143,4 +143,11 @@ struct BwdArgs {
 };
 hipError_t launch_attn_bwd_bf16(const BwdArgs& a, int head_dim, hipStream_t s);
 
+// The device-global workspace of the allocation-free backward: room for delta
+// of B * H * L <= kBwdScratchFloats rows (8 MiB per GPU). bwd_scratch_address
+// returns its address on the current device (looked up on the first call per
+// device); kernels get that address, never the symbol.
+constexpr int64_t kBwdScratchFloats = int64_t(1) << 21;
+hipError_t bwd_scratch_address(float** out);
+
 }  // namespace tmk

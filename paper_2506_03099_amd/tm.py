@@ -111,6 +111,8 @@ def lib() -> ctypes.CDLL:
                                                               ctypes.c_int32, P, P, P, P, P]),
             "tm_sparse_causal_attn_bwd": (ctypes.c_int, [D, ctypes.c_int32, P, P, P, P, P, P, P,
                                                          P, P, P, P]),
+            "tm_sparse_causal_attn_bwd_noalloc": (ctypes.c_int, [D, ctypes.c_int32, P, P, P, P, P,
+                                                                 P, P, P, P, P]),
             "tm_last_error": (ctypes.c_char_p, []),
         }
         for name, (res, args) in sig.items():
@@ -315,4 +317,14 @@ def tm_sparse_causal_attn_bwd(desc: tm_attn_desc, n_frames: int, q, k, v, o, lse
     _check(lib().tm_sparse_causal_attn_bwd(ctypes.byref(desc), n_frames, _ptr(q), _ptr(k), _ptr(v),
                                            _ptr(o), _ptr(lse), _ptr(dout), _ptr(delta), _ptr(dq),
                                            _ptr(dk), _ptr(dv), _stream(stream)))
+    return dq, dk, dv
+
+
+def tm_sparse_causal_attn_bwd_noalloc(desc: tm_attn_desc, n_frames: int, q, k, v, o, lse, dout,
+                                      dq, dk, dv, stream=None):
+    """The backward with the library's device-global workspace: the caller
+    passes every output (nothing is allocated); returns (dq, dk, dv)."""
+    _check(lib().tm_sparse_causal_attn_bwd_noalloc(ctypes.byref(desc), n_frames, _ptr(q), _ptr(k),
+                                                   _ptr(v), _ptr(o), _ptr(lse), _ptr(dout),
+                                                   _ptr(dq), _ptr(dk), _ptr(dv), _stream(stream)))
     return dq, dk, dv
