@@ -452,6 +452,9 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     bf16x8_t fr[RING];
 #pragma unroll
     for (int s = 0; s < RING; ++s) fr[s] = read_frag(s, kbuf(1), vbuf(1));
+    // Iteration 0 loads K(4) into the buffer of K(0), and a wave without rows
+    // reaches that load at once: every wave must be done reading K(0) first.
+    __syncthreads();
 
     // ---- main loop: iteration t, with x = x(t) and nx receiving S(t+1).
     // Stage 1: the score MFMAs of tile t+1, each with its share of P(t)
