@@ -59,6 +59,26 @@ def measured_traffic():
     return rec["bytes_per_launch"] if rec.get("kernel_source_sha256") == sha else None
 
 
+def device_peak_tflops(torch):
+    """Dense bf16 MFMA peak derived from the device: compute units x peak
+    shader clock x 4096 bf16 FLOP per CU per clock (one 32x32x16 bf16 MFMA,
+    32768 FLOP, per SIMD every 32 clocks, 4 SIMDs per CU); the roofline uses
+    the published 2.5 PFLOP/s."""
+    p = torch.cuda.get_device_properties(0)
+    cus = getattr(p, "multi_processor_count", 0)
+    try:  # peak clock in kHz from the HIP runtime
+        import ctypes
+        hip = ctypes.CDLL("libamdhip64.so")
+        khz = ctypes.c_int(0)
+        attr = 5  # hipDeviceAttributeClockRate, the sixth entry of hipDeviceAttribute_t
+        if hip.hipDeviceGetAttribute(ctypes.byref(khz), attr, 0) != 0 or khz.value <= 0:
+            return None
+    except OSError:
+        return None
+    return {"cus": cus, "peak_clock_mhz": round(khz.value / 1e3, 1),
+            "tflops": round(cus * khz.value * 1e3 * 4096 / 1e12, 1)}
+
+
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     p.add_argument("--gpus", type=int, default=1)
@@ -202,6 +222,7 @@ def main():
             "step": "kv append of the current chunk + one attention call",
         },
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "peak_bf16_device_tflops": device_peak_tflops(torch),
         "unmasked_tflop_per_step": round(flops / 1e12, 4),
         "attn_ms": round(attn_ms, 4),
         "attn_tflops": round(attn_tflops, 2),
@@ -254,6 +275,7 @@ def main():
     # ---------------------------------------------------------------- CPU oracle
     if args.cpu_seconds > 0:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        result["cpu_baselines"] = cpu_baselines_other(WORKLOADS, result["cpu_baseline"])
 
     print(json.dumps(result), flush=True)
 
@@ -473,6 +495,94 @@ def cpu_baseline(w, budget_s):
         "host_cpus": os.cpu_count(),
         "note": "BLAS matmuls use all threads; numpy exp/where/max are single-threaded",
     }
+
+
+def cpu_baselines_other(workloads, cfg2):
+    """The oracle on the other workloads, on the host's cores: the tiny fp32
+    workload in full; one head of the 480p full sequence (complete masked rows
+    in blocks of 2048) and one (stream, head) of the 720p chunk, each
+    extrapolated to all heads and streams (heads and streams are independent
+    problems of the same shape); the streaming loop's steady chunk as 80 calls
+    of the 480p chunk (from the timed cfg2 figure). Every extrapolation is
+    labelled."""
+    from oracle import ChunkGeometry, StreamHistory, full_sequence_attention
+    from synth import draw_chunk, draw_qkv_sequence
+    from synth.inputs import Workload
+    out = {}
+
+    def geom(w):
+        return ChunkGeometry(w.tokens_per_frame, w.chunk_frames, w.ref_frames, w.window)
+
+    # tiny fp32: 4 streamed chunks and the 9-frame sequence, all heads
+    w = workloads["tiny_f32"]
+    hist = StreamHistory(geom(w))
+    chunks = [draw_chunk(w, t) for t in range(w.n_chunks + 1)]
+    pairs = 0
+    t0 = time.perf_counter()
+    for t, c in enumerate(chunks):
+        hist.append(t, c["k"], c["v"])
+        hist.attend(c["q"], t)
+    q = np.concatenate([c["q"] for c in chunks], axis=1)
+    k = np.concatenate([c["k"] for c in chunks], axis=1)
+    v = np.concatenate([c["v"] for c in chunks], axis=1)
+    full_sequence_attention(q, k, v, geom(w))
+    dt = time.perf_counter() - t0
+    from oracle import allowed_pair_count
+    L = w.n_frames * w.tokens_per_frame
+
+    def stream_keys(t):  # c_0, then chunks max(1, t - W) .. t
+        return chunks[0]["k"].shape[1] + sum(c["k"].shape[1] for c in chunks[max(1, t - w.window):t + 1])
+
+    pairs = allowed_pair_count(L, geom(w)) + sum(c["q"].shape[1] * stream_keys(t)
+                                                 for t, c in enumerate(chunks))
+    out[w.name] = {"seconds": round(dt, 4), "kind": "oracle", "extrapolated": False,
+                   "sample": "all: 4 streamed chunks + the 9-frame sequence, 2 heads",
+                   "tflops": round(4.0 * w.head_dim * w.heads * pairs / dt / 1e12, 6)}
+
+    # 480p full sequence: one head, extrapolated to 40
+    w = workloads["wan14b_480p_full_sequence"]
+    one = Workload(w.wid, w.name, w.dtype, w.batch, 1, w.head_dim, w.tokens_per_frame,
+                   w.chunk_frames, w.ref_frames, w.window, n_frames=w.n_frames)
+    d = draw_qkv_sequence(one)
+    t0 = time.perf_counter()
+    full_sequence_attention(d["q"], d["k"], d["v"], geom(w), row_block=2048)
+    dt = time.perf_counter() - t0
+    L = w.n_frames * w.tokens_per_frame
+    pairs = allowed_pair_count(L, geom(w))
+    out[w.name] = {"seconds_one_head": round(dt, 2), "kind": "oracle", "extrapolated": True,
+                   "sample": f"1 of {w.heads} heads (32760 x 32760 masked rows in blocks of 2048); "
+                             f"ms extrapolated x{w.heads}",
+                   "ms_extrapolated": round(dt * w.heads * 1e3, 1),
+                   "tflops": round(4.0 * w.head_dim * pairs / dt / 1e12, 5)}
+    del d
+
+    # 720p chunk: one (stream, head), extrapolated to 2 streams x 40 heads
+    w = workloads["wan14b_720p_chunk_b2"]
+    one = Workload(w.wid, w.name, w.dtype, 1, 1, w.head_dim, w.tokens_per_frame, w.chunk_frames,
+                   w.ref_frames, w.window, n_chunks=w.n_chunks)
+    hist = StreamHistory(geom(w))
+    cs = [draw_chunk(one, t) for t in range(w.n_chunks + 1)]
+    for t, c in enumerate(cs):
+        hist.append(t, c["k"], c["v"])
+    n_keys = sum(c["k"].shape[1] for c in cs)
+    t0 = time.perf_counter()
+    hist.attend(cs[-1]["q"], w.n_chunks)
+    dt = time.perf_counter() - t0
+    n_q = cs[-1]["q"].shape[1]
+    out[w.name] = {"seconds_one_head": round(dt, 2), "kind": "oracle", "extrapolated": True,
+                   "sample": f"1 of {w.batch * w.heads} (stream, head) pairs ({n_q} queries x "
+                             f"{n_keys} keys); ms extrapolated x{w.batch * w.heads}",
+                   "ms_extrapolated": round(dt * w.batch * w.heads * 1e3, 1),
+                   "tflops": round(4.0 * w.head_dim * n_q * n_keys / dt / 1e12, 5)}
+
+    # streaming loop: a steady chunk is 80 calls of the 480p chunk
+    w = workloads["wan14b_480p_stream"]
+    calls = w.steps * w.layers
+    ms_call = 1.0466 / cfg2["value"]  # seconds per 480p-chunk call at the oracle's TFLOP/s
+    out[w.name] = {"kind": "oracle", "extrapolated": True,
+                   "sample": f"{calls} x the timed 480p-chunk oracle call (no separate run)",
+                   "ms_per_steady_chunk_extrapolated": round(calls * ms_call * 1e3, 1)}
+    return out
 
 
 if __name__ == "__main__":

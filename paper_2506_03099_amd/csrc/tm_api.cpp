@@ -87,13 +87,15 @@ tm_status check_desc(const tm_attn_desc* d, Geo* g) {
     g->dtype = d->dtype;
     g->elem = d->dtype == TM_BF16 ? 2 : 4;
     g->scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / std::sqrt(float(d->head_dim));
-    g->RT = g->R * g->T;
+    g->RT = g->R * g->T;  // each factor < 2^31: no overflow in 64 bits
     g->CT = g->C * g->T;
+    if (g->RT > kMaxTokens || g->CT > kMaxTokens)  // before any product of them
+        return fail(TM_E_SHAPE, "chunk too large (more than 2^30 tokens)");
     g->ref_cap = round_up(g->RT, tmk::kCacheAlign);
     g->slot_cap = round_up(g->CT, tmk::kCacheAlign);
     g->capacity = round_up(g->ref_cap + (g->W + 1) * g->slot_cap, tmk::kCacheBlock);
-    if (g->RT > kMaxTokens || g->CT > kMaxTokens || g->capacity > kMaxTokens)
-        return fail(TM_E_SHAPE, "chunk or cache too large (more than 2^30 tokens)");
+    if (g->capacity > kMaxTokens)
+        return fail(TM_E_SHAPE, "cache too large (more than 2^30 tokens)");
     if (g->B * g->H > (int64_t(1) << 20)) return fail(TM_E_SHAPE, "batch * heads too large");
     return TM_OK;
 }
