@@ -15,7 +15,8 @@
 //     Q^T held in registers for the whole loop;
 //   the softmax in fp32 on the MFMA output layout (each lane owns one query
 //     column and half of its keys): x = S*scale*log2(e) - m against a lazily
-//     raised running max m, P = exp2(x) rounded to bf16, row sums of that P;
+//     raised running max m, P = exp2(x), rounded to bf16 for the P V product,
+//     row sums of P in fp32;
 //   O^T (head_dim x queries) += V^T P^T with the same MFMA, P^T straight from
 //     registers. From the KV cache, whose V blocks are stored dimension-major,
 //     the V tile lands in LDS as V^T and each operand is one 16-byte read; the
@@ -372,7 +373,6 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     float m_run;            // running max in the scaled log2 domain (lazy)
     float l_run = 0.f;      // this lane's partial row sum
     const float c = a.scale_log2;
-    const bf16x2_t ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
     // S^T output layout: register i of block kb holds key 32*kb + (VT ?
     // 16*(i/8) + 8*hw + i%8 : 8*(i/4) + 4*hw + i%4) of the tile, query l32.
     auto key_of = [&](int kb, int i) {
@@ -396,14 +396,15 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
         return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
     };
     // P = exp2(x) for elements [e, e + 2) of x, rounded to bf16 into its P^T
-    // operand slot (k-step e/8, slot e%8), summed into *lt.
+    // operand slot (k-step e/8, slot e%8); the fp32 values are summed into *lt.
+    // (Summing the rounded pair with v_dot2_f32_bf16 instead costs more: that
+    // instruction waits for the MFMA in flight, a plain fp32 add does not.)
     auto form_p2 = [&](const f32x16_t (&x)[2], bf16x8_t (&pf)[4], int e, float& lt) __attribute__((always_inline)) {
         const float p0 = __builtin_amdgcn_exp2f(x[e >> 4][e & 15]);
         const float p1 = __builtin_amdgcn_exp2f(x[(e + 1) >> 4][(e + 1) & 15]);
         pf[e >> 3][e & 7] = static_cast<__bf16>(p0);
         pf[e >> 3][(e & 7) + 1] = static_cast<__bf16>(p1);
-        const bf16x2_t pp = {pf[e >> 3][e & 7], pf[e >> 3][(e & 7) + 1]};
-        lt = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, lt, false);
+        lt += p0 + p1;
     };
 
     // ---- prologue: tiles 0..3 of K and 0..1 of V in flight, S(0) and its

@@ -9,12 +9,12 @@ import torch
 
 # max |gpu - oracle| <= TOL * RMS(oracle output over the compared elements)
 TOL = {"f32": 1e-4, "bf16": 2e-2}
-# max |lse_gpu - lse_oracle| (natural log). The bf16 kernel sums the P it has
-# rounded to bf16 (the P that multiplies V), so its row sum l carries a
-# relative error of at most 2^-8 (half an ulp at the bottom of a binade) and
-# log l at most ln(1 + 2^-8) = 3.9e-3, reached when one key dominates the row;
-# 1e-4 covers the fp32 arithmetic around it.
-LSE_ATOL = {"f32": 1e-4, "bf16": float(np.log1p(2.0 ** -8)) + 1e-4}
+# max |lse_gpu - lse_oracle| (natural log). Both kernels form the row sum l
+# from the fp32 values of P (the bf16 kernel rounds P to bf16 only as the
+# operand of P V), and the inputs are the same values on both sides, so the
+# log-sum-exp differs from the oracle's by fp32 rounding of the logits, exp2
+# and the sums: 1e-4 covers it for either dtype.
+LSE_ATOL = {"f32": 1e-4, "bf16": 1e-4}
 
 
 def say(msg: str):

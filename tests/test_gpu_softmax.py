@@ -17,8 +17,8 @@ of 8 / sqrt(D) through the descriptor on random inputs.
 Bar: the bf16 kernel's arithmetic, through its fp32 output, within 2e-2 x RMS
 of the oracle, and its bf16 output equal to that fp32 output rounded to
 nearest even, bit for bit; fp32 within 1e-4 x RMS; the log-sum-exp within
-``LSE_ATOL`` of the oracle's (bf16: ln(1 + 2^-8) + 1e-4, the rounding of the P
-that the row sum adds up, which a peaked row with one dominant key reaches).
+``LSE_ATOL`` (1e-4) of the oracle's: the row sums are formed in fp32 from the
+unrounded P.
 """
 import numpy as np
 import pytest
