@@ -105,9 +105,9 @@ struct AudioArgs {
 constexpr int kAudioBlocksPerPart = 32;
 
 // LDS of one audio workgroup: a window of nk_pad keys as K rows and V rows of
-// D bf16 each, then the face ids of the workgroup's rows and one word per
-// wave.
-constexpr size_t kAudioFaceLds = 4 * 32 * kAudioBlocksPerPart + 4 * 8;
+// D bf16 each, then the face ids of the workgroup's rows, one word per wave,
+// the rows of one stream compacted (16-bit indices) and their count.
+constexpr size_t kAudioFaceLds = 4 * 32 * kAudioBlocksPerPart + 4 * 8 + 2 * 32 * kAudioBlocksPerPart + 16;
 __host__ __device__ constexpr size_t audio_lds_bytes(int head_dim, int nk_pad) {
     return 2 * static_cast<size_t>(nk_pad) * head_dim * 2 + kAudioFaceLds;
 }
