@@ -267,8 +267,8 @@ typedef struct tm_audio_desc {
  * but must not otherwise overlap q, ak, av or face.
  * A frame's window (at most (2w + 1) * A keys, rounded up to 32) must fit in
  * one workgroup's LDS: at most 288 keys at D = 128, 608 at D = 64, else
- * TM_E_SHAPE. n_tok = 0 launches nothing. P is rounded to bf16 before P V and
- * the row sums use the rounded P; the result is deterministic. */
+ * TM_E_SHAPE. n_tok = 0 launches nothing. P is rounded to bf16 before P V;
+ * the row sums add the fp32 P. The result is deterministic. */
 tm_status tm_audio_cross_attn_fwd(const tm_audio_desc* desc, const void* q, int32_t first_frame,
                                   int32_t n_tok, const void* ak, const void* av,
                                   const int32_t* face, void* o, hipStream_t stream);
