@@ -72,6 +72,13 @@ __device__ __forceinline__ void wait_lds_dma_but() {
 // takes x as input and output, so the computation of x cannot be moved past
 // it (the compiler would otherwise sink work that is only used after a branch
 // or a barrier, away from the MFMAs it is meant to overlap).
+// threadIdx.x, which the compiler cannot fold into an earlier copy.
+__device__ __forceinline__ int fresh_thread_index() {
+    int v = static_cast<int>(threadIdx.x);
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
 __device__ __forceinline__ float pin(float x) {
     asm volatile("" : "+v"(x));
     return x;
@@ -262,9 +269,13 @@ __global__ __launch_bounds__(kBf16Threads, 1) void attn_fwd_bf16_kernel(const At
     // last, so they are planned again only for a range's last tile and for the
     // tile after it.
     auto plan = [&](uint32_t (&off)[NI], bool is_v, const KeyTile& t) __attribute__((always_inline)) {
+        // the thread index read afresh: the per-lane terms below are then
+        // recomputed on this rare path instead of being kept live (spilled)
+        // across the key loop
+        const int tix = fresh_thread_index();
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
-            const int ch = (i * NW + wave) * 64 + lane;
+            const int ch = i * kBf16Threads + tix;
             if (!is_v || !VT) {
                 const int row = min(ch / CPR, t.ke - 1 - t.k0);
                 const int gc = (ch % CPR) ^ lds_swizzle<D>(ch / CPR);
