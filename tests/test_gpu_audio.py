@@ -11,7 +11,8 @@ the bf16 format alone comes close to the bar.) Rows without a face, and rows
 whose face id is outside [0, M), must be exactly zero in both outputs. Cases: ragged row blocks and a partial last frame, windows clipped at
 both ends of the audio, a window padded to the next 32 keys, several streams
 mixed inside one 32-row block, frames split over several workgroups, the
-largest window that fits in LDS, in-place output, no rows, and the 480p
+largest window that fits in LDS, in-place output, no rows, rows that use no
+stream 0, more dense face blocks than compute waves, and the 480p
 workloads (two faces in full, one face on sampled heads and rows).
 """
 import numpy as np
@@ -95,6 +96,22 @@ def test_audio_matches_oracle_small(tm, D, first):
     desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
     o = _run(tm, desc, qd, first, akd, avd, torch.from_numpy(face).cuda())
     _check(o, q, ak, av, face, T, A, first, w, f"D={D} first={first}")
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_audio_stream_zero_unused_and_many_face_blocks(tm, D):
+    """Rows of streams 1 and 2 only (the kernel's window loads for stream 0,
+    issued before the face ids are known, are dropped), and a frame whose rows
+    are nearly all faces (more dense 32-row blocks than compute waves)."""
+    B, H, T, A, Fa, M, w, frames = 1, 2, 700, 16, 8, 3, 2, 3
+    say(f"audio without stream 0: D={D}")
+    n = T * frames
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(300 + D, B, n, H, D, M, Fa * A)
+    face = rng.choice([-1, 1, 2], size=(B, n), p=[0.3, 0.35, 0.35]).astype(np.int32)
+    face[:, T:2 * T] = np.where(rng.random((B, T)) < 0.95, 2, -1)  # frame 1: one stream, 95% of rows
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = _run(tm, desc, qd, 1, akd, avd, torch.from_numpy(face).cuda())
+    _check(o, q, ak, av, face, T, A, 1, w, f"no stream 0 D={D}")
 
 
 @pytest.mark.parametrize("T,A,n_extra", [(70, 32, 35), (1100, 33, 100), (2100, 32, 0)])
