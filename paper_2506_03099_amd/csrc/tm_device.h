@@ -47,6 +47,8 @@ __device__ __forceinline__ int lds_swizzle(int row) {
 
 // s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
 constexpr int kWaitVmcnt0 = 0x0F70;
+// s_waitcnt immediate for lgkmcnt(0), vmcnt and expcnt unconstrained.
+constexpr int kWaitLgkmcnt0 = 0xC07F;
 
 // A pointer that is the same in every lane, held in scalar registers.
 __device__ __forceinline__ const void* uniform_ptr(const void* p) {
@@ -99,6 +101,21 @@ __device__ __forceinline__ void lds_dma4x2(const void* sbase0, uint32_t voff0, u
         "s_nop 0"
         : "=&s"(saved)
         : "s"(lds0), "v"(voff0), "s"(sbase0), "s"(lds1), "v"(voff1), "s"(sbase1));
+}
+
+// One direct global->LDS load (global_load_lds_dwordx4) of 16 bytes per lane
+// into lds + 16 * l, as lds_dma16x2 otherwise.
+__device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\t"
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0"
+        : "=&s"(saved)
+        : "s"(lds), "v"(voff), "s"(sbase));
 }
 
 // Wait until every direct global->LDS load issued by this wave has written

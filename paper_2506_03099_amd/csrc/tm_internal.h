@@ -98,18 +98,26 @@ struct AudioArgs {
     int32_t max_keys_pad;  // most window keys of any frame, rounded up to 32
     int32_t o_f32;         // store o as fp32 (the values before the final rounding)
     float scale_log2;      // softmax scale * log2(e)
+    int32_t n_cwg;         // compute workgroups (B * H * n_frames * parts); set by the launcher
+    int32_t zrows;         // token rows per zero-fill workgroup; set by the launcher
+    int32_t q_stage;       // queries (and bf16 output rows) staged in LDS; set by the launcher
 };
 
 // Most 32-row blocks of one frame per audio workgroup: a frame with more
 // blocks is split over several workgroups, which take every parts-th block.
-constexpr int kAudioBlocksPerPart = 32;
+constexpr int kAudioBlocksPerPart = 64;
 
 // LDS of one audio workgroup: a window of nk_pad keys as K rows and V rows of
-// D bf16 each, then the face ids of the workgroup's rows, one word per wave,
-// the rows of one stream compacted (16-bit indices) and their count.
-constexpr size_t kAudioFaceLds = 4 * 32 * kAudioBlocksPerPart + 4 * 8 + 2 * 32 * kAudioBlocksPerPart + 16;
+// D bf16 each, then one word per wave (8), the face waves' row counts per
+// segment (32), the count of one stream's rows (one word, padded to 16 bytes)
+// and those rows compacted (16-bit indices). Staging the queries and the
+// output through LDS adds one slot of 32 rows of D bf16 per wave.
+constexpr size_t kAudioFaceLds = 4 * 8 + 4 * 32 + 16 + 2 * 32 * kAudioBlocksPerPart;
 __host__ __device__ constexpr size_t audio_lds_bytes(int head_dim, int nk_pad) {
     return 2 * static_cast<size_t>(nk_pad) * head_dim * 2 + kAudioFaceLds;
+}
+__host__ __device__ constexpr size_t audio_stage_lds_bytes(int head_dim) {
+    return static_cast<size_t>(8) * 32 * head_dim * 2;
 }
 constexpr size_t kAudioMaxLds = 160 * 1024;  // gfx950: 160 KiB of LDS per workgroup
 // Most window keys (a multiple of 32) that fit: 288 at D = 128, 608 at D = 64.
