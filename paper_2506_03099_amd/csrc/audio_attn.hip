@@ -384,23 +384,26 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
 #pragma unroll
                 for (int d = 0; d < DB; ++d) acc[d] *= alpha;
             }
+            // P rounded to bf16 for the P V product; the row sums add the fp32
+            // P. P of tile u + 1 is formed while the P V MFMAs of tile u run:
+            // each of those MFMAs is followed by two of its elements (tiles
+            // past the window give P = 0).
+            float lsum = 0.f;
+            auto p_pair = [&](int u, int i, bf16x8_t (&pn)[2]) __attribute__((always_inline)) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[u][i], c, -m_run));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[u][i + 1], c, -m_run));
+                pn[i / 8][i % 8] = static_cast<__bf16>(p0);
+                pn[i / 8][i % 8 + 1] = static_cast<__bf16>(p1);
+                lsum += p0 + p1;
+            };
+            bf16x8_t pf[2];
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) p_pair(0, i, pf);
 #pragma unroll
             for (int u = 0; u < kGroup; ++u) {
                 if (g0 + u >= ntile) break;
                 const uint32_t tile = (g0 + u) * 32 * ROWB;
-                // P rounded to bf16 for the P V product; the row sums add the fp32 P
-                bf16x8_t pf[2];
-                float l0 = 0.f, l1 = 0.f;
-#pragma unroll
-                for (int i = 0; i < 16; i += 2) {
-                    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[u][i], c, -m_run));
-                    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[u][i + 1], c, -m_run));
-                    pf[i / 8][i % 8] = static_cast<__bf16>(p0);
-                    pf[i / 8][i % 8 + 1] = static_cast<__bf16>(p1);
-                    l0 += p0;
-                    l1 += p1;
-                }
-                l_run += l0 + l1;
+                bf16x8_t pn[2];
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int jj = 0; jj < 2; ++jj) {
@@ -415,10 +418,21 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
                         vf[d] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
                     }
 #pragma unroll
-                    for (int d = 0; d < DB; ++d)
+                    for (int d = 0; d < DB; ++d) {
                         acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[d], pf[jj], acc[d], 0, 0, 0);
+                        if (u + 1 < kGroup) {
+#pragma unroll
+                            for (int q = 0; q < 4 / DB; ++q) p_pair(u + 1, 2 * ((jj * DB + d) * (4 / DB) + q), pn);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+                if (u + 1 < kGroup) {
+                    pf[0] = pn[0];
+                    pf[1] = pn[1];
                 }
             }
+            l_run += lsum;
         }
         const auto lsw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run),
                                                           false, false);
