@@ -123,7 +123,7 @@ __device__ __forceinline__ void zero_fill_rows(const AudioArgs& a, int z, lds_u8
             for (int u = 0; u < ZB; ++u) {
                 const int i = i0 + u * kAudioThreads;
                 if (i < n_chunks && fz[u] == 0)
-                    *reinterpret_cast<u32x4_t*>(base + static_cast<int64_t>(i) * 16) = u32x4_t{0, 0, 0, 0};
+                    store16_through(base + static_cast<int64_t>(i) * 16, u32x4_t{0, 0, 0, 0});
             }
         }
     }
@@ -462,7 +462,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
                     const u32x4_t v = *(lds_u32x4_t*)(slot + cidx * 16);
                     if (32 * jb + r < nf) {
                         const int tok = part_row(static_cast<int>(list_l[32 * jb + r]));
-                        *reinterpret_cast<u32x4_t*>(ob + tok * st * 2 + ((pos ^ lds_swizzle<D>(r)) << 4)) = v;
+                        store16_through(ob + tok * st * 2 + ((pos ^ lds_swizzle<D>(r)) << 4), v);
                     }
                 }
                 asm volatile("" ::: "memory");  // the slot is free once these reads are done

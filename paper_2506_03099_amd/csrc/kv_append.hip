@@ -29,6 +29,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "tm_device.h"
 #include "tm_internal.h"
 
 namespace tmk {
@@ -207,9 +208,14 @@ __global__ __launch_bounds__(kAppendThreads) void kv_write_kernel(
             rms_normalise_row<EB, D, VPR>(xq, gq, eps);
             rms_normalise_row<EB, D, VPR>(xk, gk, eps);
             kv[it] = pack16<EB>(xk);
-            if (has_src) *reinterpret_cast<uint4*>(q_out + head_off + src * src_stride + c * 16) = pack16<EB>(xq);
+            if (has_src) {
+                const uint4 w = pack16<EB>(xq);
+                store16_through(q_out + head_off + src * src_stride + c * 16, u32x4_t{w.x, w.y, w.z, w.w});
+            }
         }
-        if (has_src) *reinterpret_cast<uint4*>(k_pool + (head * capacity + row) * ROWB + c * 16) = kv[it];
+        if (has_src)
+            store16_through(k_pool + (head * capacity + row) * ROWB + c * 16,
+                            u32x4_t{kv[it].x, kv[it].y, kv[it].z, kv[it].w});
         if (in_block) {
             uint32_t* t = &tile[r * PITCH + c * 4];
             t[0] = vv[it].x;
@@ -240,8 +246,7 @@ __global__ __launch_bounds__(kAppendThreads) void kv_write_kernel(
                 w[e] = (a0 & 0xFFFFu) | (a1 << 16);
             }
         }
-        *reinterpret_cast<uint4*>(vblk + (static_cast<int64_t>(d) * B64 + g * TPG) * EB) =
-            make_uint4(w[0], w[1], w[2], w[3]);
+        store16_through(vblk + (static_cast<int64_t>(d) * B64 + g * TPG) * EB, u32x4_t{w[0], w[1], w[2], w[3]});
     }
 }
 

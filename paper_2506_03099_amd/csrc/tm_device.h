@@ -118,6 +118,17 @@ __device__ __forceinline__ void lds_dma16(const void* sbase, uint32_t voff, uint
         : "s"(lds), "v"(voff), "s"(sbase));
 }
 
+// 16-byte store at system scope (sc0 sc1), written through the L2. A plain
+// store leaves its line dirty in the L2, and the dirty lines are written back
+// when the kernel ends, after its last wave: for a kernel whose output is
+// mostly stores (tens of MB) that is a serial tail of a few
+// microseconds, where written-through lines drain while the kernel runs. The
+// s_nop covers the store reading its data registers after issue.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store16_through(void* p, u32x4_t v) {
+    asm volatile("global_store_dwordx4 %0, %1, off sc0 sc1\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
+}
+
 // Wait until every direct global->LDS load issued by this wave has written
 // LDS. The barrier that publishes a tile only orders LDS operations; the
 // direct loads count as vector-memory operations, so each wave waits for its
