@@ -114,11 +114,12 @@ def test_audio_stream_zero_unused_and_many_face_blocks(tm, D):
     _check(o, q, ak, av, face, T, A, 1, w, f"no stream 0 D={D}")
 
 
-@pytest.mark.parametrize("T,A,n_extra", [(70, 32, 35), (1100, 33, 100), (2100, 32, 0)])
+@pytest.mark.parametrize("T,A,n_extra", [(70, 32, 35), (1100, 33, 100), (2100, 32, 0), (4200, 32, 50)])
 def test_audio_ragged_rows_split_frames_and_padded_windows(tm, T, A, n_extra):
-    # T = 70: blocks of 32, 32, 6 rows; T = 1100: 35 blocks, two workgroups per
-    # frame taking every other block; T = 2100: 66 blocks, three workgroups;
-    # A = 33: 165 keys padded to 192; a partial last frame
+    # T = 70: blocks of 32, 32, 6 rows; T = 1100: 35 blocks, one workgroup per
+    # frame; T = 2100: 66 blocks, two workgroups per frame taking every other
+    # block; T = 4200: 132 blocks, three workgroups; A = 33: 165 keys padded to
+    # 192; a partial last frame
     B, H, D, Fa, M, w, first = 1, 2, 128, 6, 2, 2, 1
     n = 2 * T + n_extra
     say(f"audio ragged: T={T} A={A} n={n}")
