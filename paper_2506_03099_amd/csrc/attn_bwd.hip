@@ -51,19 +51,8 @@ typedef __attribute__((address_space(3))) float lds_f32;
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
 
-// Position of 16-byte chunk c of row `row` in the LDS tiles of both gradient
-// kernels (K and V in dQ; Q, dO and V in dK/dV): c ^ bwd_swizzle<D>(row).
-// LDS serves 64 banks of 4 bytes: a 16-byte read per lane covers 16 lanes per
-// cycle (16 consecutive rows of one chunk: distinct chunk slots), an 8-byte
-// transposing read 32 lanes (4 consecutive rows, 4 chunks each: distinct
-// 64-byte slot groups). D = 128: a permutation of 0..15 over 16 rows whose
-// bits 2-3 differ over 4 aligned rows; D = 64 (two rows per 256 bytes): the
-// same within the even and within the odd rows.
-template <int D>
-__device__ __forceinline__ int bwd_swizzle(int row) {
-    return D == 128 ? 4 * (row & 3) + ((row >> 2) & 3) : 4 * ((row >> 1) & 1) + ((row >> 2) & 3);
-}
-
+// LDS tiles of both gradient kernels (K and V in dQ; Q, dO and V in dK/dV)
+// put 16-byte chunk c of row `row` at c ^ tr_swizzle<D>(row).
 // Per-lane LDS byte offsets inside such a tile (rows at multiples of 16 keep
 // the pattern):
 // - row operand (A of S^T = K Q^T, or A of S = Q K^T): row l32, chunk
@@ -84,13 +73,13 @@ struct TileBases {
     uint32_t row0, tr0, tr8;
     __device__ __forceinline__ TileBases(int lane) {
         const int l32 = lane & 31, hw = lane >> 5;
-        row0 = l32 * ROWB + ((hw ^ bwd_swizzle<D>(l32)) << 4);
+        row0 = l32 * ROWB + ((hw ^ tr_swizzle<D>(l32)) << 4);
         const int grp = lane >> 4, gi = lane & 15;
         const int r = 4 * hw + (gi >> 2);
         const int cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
         const int half = (gi & 1) * 8;
-        tr0 = r * ROWB + ((cbase ^ bwd_swizzle<D>(r)) << 4) + half;
-        tr8 = r * ROWB + ((cbase ^ bwd_swizzle<D>(r + 8)) << 4) + half;
+        tr0 = r * ROWB + ((cbase ^ tr_swizzle<D>(r)) << 4) + half;
+        tr8 = r * ROWB + ((cbase ^ tr_swizzle<D>(r + 8)) << 4) + half;
     }
     __device__ __forceinline__ TileBases pinned() const {
         TileBases t = *this;
@@ -282,7 +271,7 @@ __global__ __launch_bounds__(kDqThreads, 2) void bwd_dq_kernel(const BwdArgs a) 
             const int blk = i * NW + wave;
             const int ch = blk * 64 + lane;
             const int row = ch / CPR;
-            const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
+            const int gc = (ch % CPR) ^ tr_swizzle<D>(row);
             const uint32_t voff = static_cast<uint32_t>((min(row, last) * st + gc * 8) * 2);
             const uint32_t l = lds_base + u * BUF + blk * 1024;
             lds_dma16x2(ks, voff, l, vs, voff, l + KT);
@@ -458,7 +447,7 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
             const int blk = i * NW + wave;
             const int ch = blk * 64 + lane;
             const int row = ch / CPR;
-            const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
+            const int gc = (ch % CPR) ^ tr_swizzle<D>(row);
             const uint32_t voff = static_cast<uint32_t>((min(row, last) * st + gc * 8) * 2);
             const uint32_t l = lds_base + u * STAGE + blk * 1024;
             lds_dma16x2(qs, voff, l, ds, voff, l + TILE);
@@ -492,7 +481,7 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
             for (int m = 0; m < 2; ++m) {
                 const int ch = (i + m) * 64 + lane;
                 const int row = ch / CPR;
-                const int gc = (ch % CPR) ^ bwd_swizzle<D>(row);
+                const int gc = (ch % CPR) ^ tr_swizzle<D>(row);
                 vo[m] = static_cast<uint32_t>((min(row, vlast) * st + gc * 8) * 2);
             }
             const uint32_t l = lds_base + VT + wave * 32 * ROWB + i * 1024;

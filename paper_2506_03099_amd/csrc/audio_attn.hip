@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
         for (int i = wave; i < n_instr; i += NCW) {
             const int c = 64 * i + lane;
             const int k = c / CPR, pos = c % CPR;
-            const int gc = pos ^ lds_swizzle<D>(k);
+            const int gc = pos ^ tr_swizzle<D>(k);
             const uint32_t off = static_cast<uint32_t>((min(k, nk - 1) * st + gc * 8) * 2);
             const uint32_t l = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(64 * i * 16));
             lds_dma16x2(kg, off, lds_k + l, vg, off, lds_v + l);
@@ -268,7 +268,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
     // P^T element for step i/8, slot i%8, matches the V^T row order.
     uint32_t koff[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) koff[kk] = l32 * ROWB + (((2 * kk + hw) ^ lds_swizzle<D>(l32)) << 4);
+    for (int kk = 0; kk < KK; ++kk) koff[kk] = l32 * ROWB + (((2 * kk + hw) ^ tr_swizzle<D>(l32)) << 4);
     const int grp = lane >> 4, gi = lane & 15;
     const int v_row = 4 * hw + (gi >> 2);
     const int v_cbase = 2 * (grp & 1) + ((gi & 3) >> 1);
@@ -277,8 +277,8 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
         const int cc = 4 * d + v_cbase;
-        voff[2 * d] = v_row * ROWB + ((cc ^ lds_swizzle<D>(v_row)) << 4) + v_half;
-        voff[2 * d + 1] = (v_row + 8) * ROWB + ((cc ^ lds_swizzle<D>(v_row + 8)) << 4) + v_half;
+        voff[2 * d] = v_row * ROWB + ((cc ^ tr_swizzle<D>(v_row)) << 4) + v_half;
+        voff[2 * d + 1] = (v_row + 8) * ROWB + ((cc ^ tr_swizzle<D>(v_row + 8)) << 4) + v_half;
     }
 
     // Query fragments of row `row`: lane l32's row, the half-wave's k-slices.
@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
         for (int i = 0; i < 32 * CPR / 64; ++i) {
             const int cidx = 64 * i + lane;
             const int r = cidx / CPR, pos = cidx % CPR;
-            const int gc = pos ^ lds_swizzle<D>(r);
+            const int gc = pos ^ tr_swizzle<D>(r);
             const int tok = part_row(static_cast<int>(list_l[min(32 * jb + r, nf - 1)]));
             const uint32_t off = static_cast<uint32_t>((tok * st + gc * 8) * 2);
             lds_dma16(qs, off, static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(lds_slot + 64 * i * 16)));
@@ -451,7 +451,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
                         bf16x4_t w;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(acc[d][4 * g + e] * inv);
-                        *(lds_bf16x4_t*)(slot + r32 * ROWB + (((4 * d + g) ^ lds_swizzle<D>(r32)) << 4) + h2 * 8) = w;
+                        *(lds_bf16x4_t*)(slot + r32 * ROWB + (((4 * d + g) ^ tr_swizzle<D>(r32)) << 4) + h2 * 8) = w;
                     }
                 }
                 asm volatile("" ::: "memory");
@@ -462,7 +462,7 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
                     const u32x4_t v = *(lds_u32x4_t*)(slot + cidx * 16);
                     if (32 * jb + r < nf) {
                         const int tok = part_row(static_cast<int>(list_l[32 * jb + r]));
-                        store16_through(ob + tok * st * 2 + ((pos ^ lds_swizzle<D>(r)) << 4), v);
+                        store16_through(ob + tok * st * 2 + ((pos ^ tr_swizzle<D>(r)) << 4), v);
                     }
                 }
                 asm volatile("" ::: "memory");  // the slot is free once these reads are done

@@ -45,6 +45,19 @@ __device__ __forceinline__ int lds_swizzle(int row) {
     return D == 128 ? low + 8 * ((row >> 3) & 1) : low;
 }
 
+// Position of 16-byte chunk c of row `row` in an LDS tile of D bf16 per row
+// read both by rows and by transposing reads: c ^ tr_swizzle<D>(row). LDS
+// serves 64 banks of 4 bytes: a 16-byte read per lane covers 16 lanes per
+// cycle (16 consecutive rows of one chunk: distinct chunk slots), an 8-byte
+// transposing read 32 lanes (4 consecutive rows, 4 chunks each: distinct
+// 64-byte slot groups). D = 128: a permutation of 0..15 over 16 rows whose
+// bits 2-3 differ over 4 aligned rows; D = 64 (two rows per 256 bytes): the
+// same within the even and within the odd rows.
+template <int D>
+__device__ __forceinline__ int tr_swizzle(int row) {
+    return D == 128 ? 4 * (row & 3) + ((row >> 2) & 3) : 4 * ((row >> 1) & 1) + ((row >> 2) & 3);
+}
+
 // s_waitcnt immediate (gfx9 encoding) for vmcnt(0), expcnt and lgkmcnt unconstrained.
 constexpr int kWaitVmcnt0 = 0x0F70;
 // s_waitcnt immediate for lgkmcnt(0), vmcnt and expcnt unconstrained.
