@@ -508,15 +508,26 @@ __global__ __launch_bounds__(kDkdvThreads, 2) void bwd_dkdv_kernel(const BwdArgs
         const lds_f32* ls = (const lds_f32*)(L + VEC + U * 256);
         const lds_f32* dls = (const lds_f32*)(L + VEC + 512 + U * 256);
         const TileBases<D> off = tb.pinned();
-        // the two chains interleaved: one's MFMA covers the other's LDS reads
+        // the two chains interleaved: one's MFMA covers the other's LDS reads;
+        // the operands of k-step kk + 2 are read while k-step kk runs
         f32x16_t s = f32x16_t{}, dp = f32x16_t{};
+        bf16x8_t qa[3], da[3], vb[3];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            qa[kk] = *(const lds_bf16x8_t*)(Qb + off.row(kk));
+            da[kk] = *(const lds_bf16x8_t*)(Db + off.row(kk));
+            vb[kk] = *(const lds_bf16x8_t*)(Vw + off.row(kk));
+        }
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-            const bf16x8_t qa = *(const lds_bf16x8_t*)(Qb + off.row(kk));
-            const bf16x8_t da = *(const lds_bf16x8_t*)(Db + off.row(kk));
-            const bf16x8_t vb = *(const lds_bf16x8_t*)(Vw + off.row(kk));
-            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[kk], s, 0, 0, 0);
-            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dp, 0, 0, 0);
+            if (kk + 2 < KK) {
+                qa[(kk + 2) % 3] = *(const lds_bf16x8_t*)(Qb + off.row(kk + 2));
+                da[(kk + 2) % 3] = *(const lds_bf16x8_t*)(Db + off.row(kk + 2));
+                vb[(kk + 2) % 3] = *(const lds_bf16x8_t*)(Vw + off.row(kk + 2));
+            }
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[kk % 3], kf[kk], s, 0, 0, 0);
+            dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[kk % 3], vb[kk % 3], dp, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
         // P and dS, 4 consecutive queries at a time (their lse, +inf for rows
         // past qend so that P = 0, and delta)
