@@ -12,7 +12,8 @@ whose face id is outside [0, M), must be exactly zero in both outputs. Cases: ra
 both ends of the audio, a window padded to the next 32 keys, several streams
 mixed inside one 32-row block, frames split over several workgroups, the
 largest window that fits in LDS, in-place output, no rows, rows that use no
-stream 0, more dense face blocks than compute waves, and the 480p
+stream 0, more dense face blocks than compute waves (with the queries staged in
+LDS and, for windows too long for that, gathered into registers), and the 480p
 workloads (two faces in full, one face on sampled heads and rows).
 """
 import numpy as np
@@ -112,6 +113,25 @@ def test_audio_stream_zero_unused_and_many_face_blocks(tm, D):
     desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
     o = _run(tm, desc, qd, 1, akd, avd, torch.from_numpy(face).cuda())
     _check(o, q, ak, av, face, T, A, 1, w, f"no stream 0 D={D}")
+
+
+@pytest.mark.parametrize("D,A", [(128, 40), (64, 100)])
+def test_audio_unstaged_queries_many_streams_and_blocks(tm, D, A):
+    """Windows too long for the per-wave query slots beside them in LDS
+    (200 keys at D = 128, 500 at D = 64): queries gathered into registers and
+    outputs stored from them, with three streams, rows of stream 0 missing in
+    one frame and a frame whose rows are nearly all one face (more dense blocks
+    than waves, so waves gather a second block)."""
+    B, H, T, Fa, M, w, frames = 1, 2, 700, 8, 3, 2, 3
+    say(f"audio unstaged: D={D} keys={5 * A}")
+    n = T * frames
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(600 + D, B, n, H, D, M, Fa * A)
+    face = rng.choice([-1, 0, 1, 2], size=(B, n), p=[0.25, 0.25, 0.25, 0.25]).astype(np.int32)
+    face[:, T:2 * T] = np.where(rng.random((B, T)) < 0.95, 1, -1)
+    face[:, 2 * T:] = np.where(face[:, 2 * T:] == 0, 2, face[:, 2 * T:])
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = _run(tm, desc, qd, 2, akd, avd, torch.from_numpy(face).cuda())
+    _check(o, q, ak, av, face, T, A, 2, w, f"unstaged D={D}")
 
 
 @pytest.mark.parametrize("T,A,n_extra", [(70, 32, 35), (1100, 33, 100), (2100, 32, 0), (4200, 32, 50)])
