@@ -13,7 +13,8 @@ both ends of the audio, a window padded to the next 32 keys, several streams
 mixed inside one 32-row block, frames split over several workgroups, the
 largest window that fits in LDS, in-place output, no rows, rows that use no
 stream 0, more dense face blocks than compute waves (with the queries staged in
-LDS and, for windows too long for that, gathered into registers), and the 480p
+LDS and, for windows too long for that, gathered into registers), more rows
+than one zero-fill workgroup stages at once, and the 480p
 workloads (two faces in full, one face on sampled heads and rows).
 """
 import numpy as np
@@ -224,6 +225,25 @@ def test_audio_480p_two_faces_full(tm):
              torch.from_numpy(d["face"]).cuda())
     _check(o, d["q"], d["ak"], d["av"], d["face"], w.tokens_per_frame, w.audio_per_frame,
            w.first_frame, w.half_window, w.name)
+
+
+def test_audio_many_rows_zero_fill_in_batches(tm):
+    """More compute workgroups than CUs (8 heads x 40 frames) and 40000 rows:
+    each zero-fill workgroup covers more rows than one batch of face flags
+    (512), so it stages several batches. Every row without a face must be
+    zero in all heads; face rows are compared on a sample."""
+    B, H, D, T, A, M, w, frames = 1, 8, 64, 1000, 16, 2, 2, 40
+    n = T * frames
+    Fa = frames + 2
+    say(f"audio many rows: n={n}, {H} heads")
+    rng, (q, ak, av), (qd, akd, avd) = _inputs(77, B, n, H, D, M, Fa * A)
+    face = rng.choice([-1, 0, 1, 5], size=(B, n), p=[0.55, 0.2, 0.2, 0.05]).astype(np.int32)
+    desc = tm.make_audio_desc(B, H, D, T, A, Fa, M, w)
+    o = _run(tm, desc, qd, 1, akd, avd, torch.from_numpy(face).cuda())
+    on = torch.from_numpy((face >= 0) & (face < M)).cuda()
+    assert bool((o[0][~on] == 0).all()) and bool((o[1][~on] == 0).all()), "rows without a face are not zero"
+    rows = np.sort(rng.choice(n, 400, replace=False))
+    _check(o, q, ak, av, face, T, A, 1, w, "many rows", heads=[0, 5, 7], rows=rows)
 
 
 def test_audio_480p_chunk_sampled(tm):
