@@ -145,6 +145,8 @@ __global__ __launch_bounds__(kAudioThreads) void audio_attn_bf16_kernel(const Au
     constexpr int FT = NFW * 64;  // threads of the face waves
     constexpr int FID = 32 * kAudioBlocksPerPart / FT;  // face ids per face-wave thread
     static_assert(FID * FT == 32 * kAudioBlocksPerPart, "face ids must tile the face waves");
+    static_assert(4 * (kAudioWaves + FID * NFW + 4) + 2 * 32 * kAudioBlocksPerPart == kAudioFaceLds,
+                  "the LDS carve-up below must match kAudioFaceLds");
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
